@@ -1,0 +1,275 @@
+/*
+ * compass.h — C ABI of the MI355X implementation of the Compass hot path.
+ *
+ * Compass (arXiv 2609.10549) hides tensor-parallel communication behind GEMM
+ * work in two ways: IntraFusion, one fused operator whose output tiles run in
+ * the order their input chunks arrive over a single or double ring
+ * (Section III), and InterDecom, d pipelined sub-operators (Section II-B,
+ * Section IV). An analytic model picks the degree d and the strategy
+ * (Section IV-C, Section V, Algorithm 1).
+ *
+ * This library implements one tensor-parallel rank's share of both operators
+ * on a single GPU. The other ranks are emulated: their shards / partial sums
+ * live in separate device allocations or in pinned host memory, and SDMA copy
+ * engines move them into this rank's buffers at configurable per-ring link
+ * rates, publishing per-partition arrival flags that the GEMM kernel polls.
+ *
+ * Conventions
+ *   - bf16 data is passed as raw 16-bit patterns (uint16); fp32 as float.
+ *   - Every matrix is row-major and densely packed (leading dimension = its
+ *     column count).
+ *   - The GEMM computes C = A * B with B = W^T, where W is N x K (the Linear
+ *     weight layout: K contiguous for both operands). Products accumulate in
+ *     fp32; C is rounded once to bf16, nearest-even.
+ *   - "device" pointers are HIP device allocations of the current device;
+ *     "pinned host" pointers come from hipHostMalloc. Every buffer is owned by
+ *     the caller; the library keeps only a small control block per device
+ *     (flags, counters, copy-engine state), allocated on first use.
+ *   - Calls are stream-ordered on the stream passed in (a hipStream_t; NULL is
+ *     the default stream). Operations of this library must not overlap on one
+ *     device: they share the control block. Issue them from one host thread.
+ *   - Every entry point returns COMPASS_OK (0) or a negative status; the
+ *     message of the last failure on the calling thread is returned by
+ *     compass_last_error(). Argument checks happen before anything is
+ *     enqueued. A kernel-side wait that exceeds its bound is reported as
+ *     COMPASS_ERR_TIMEOUT by the next call or by compass_sync().
+ */
+#ifndef COMPASS_H
+#define COMPASS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define COMPASS_OK               0
+#define COMPASS_ERR_INVALID     -1  /* bad argument (shape, pointer, rank...) */
+#define COMPASS_ERR_UNSUPPORTED -2  /* valid but outside what is implemented  */
+#define COMPASS_ERR_HIP         -3  /* HIP / HSA runtime call failed          */
+#define COMPASS_ERR_TIMEOUT     -4  /* a bounded wait (flag, copy) expired    */
+
+/* ---- enumerations ------------------------------------------------------ */
+#define COMPASS_AG_GEMM   0  /* AllGather + GEMM      (Section II-A, Fig. 1) */
+#define COMPASS_GEMM_RS   1  /* GEMM + ReduceScatter  (Section II-A, Fig. 1) */
+
+#define COMPASS_RING_SINGLE 0  /* one ring, n-1 steps of m/n (Section III-A) */
+#define COMPASS_RING_DOUBLE 1  /* two counter-rotating rings, each chunk split
+                                  into a forward and a backward half
+                                  (Section III-A, Fig. 5(b); III-B, Fig. 6) */
+
+#define COMPASS_INTRA_FUSION 0  /* TA-IntraFusion  (Algorithm 1) */
+#define COMPASS_INTER_DECOM  1  /* ODP-InterDecom  (Algorithm 1) */
+
+/* ---- ring schedule (Section III-A, III-B) -------------------------------
+ * Writes the order in which rank `rank` of an n-rank ring processes the
+ * chunks (single ring: chunk ids 0..n-1) or partitions (double ring:
+ * partition p = 2c + h, h = 0 for the first row half of chunk c, carried by
+ * the backward ring, h = 1 for the second half, forward ring).
+ *   AllGather:      local data first, then arrivals step by step; under the
+ *                   double ring the forward-ring partition precedes the
+ *                   backward-ring one within a step.
+ *   ReduceScatter:  textbook ring order (r-1-s) mod n, local chunk last.
+ * `out` receives `cap` >= n (single) or 2n (double) int32 entries.
+ * Returns the number of entries written, or a negative status.
+ * Host only; needs no GPU. */
+int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int cap);
+
+/* ---- emulated links -----------------------------------------------------
+ * Rates are the emulated per-direction link bandwidths of the two rings
+ * (bytes per second). A single ring uses fwd_Bps only. A rate <= 0 means
+ * "unpaced" (copies go out as fast as the engines take them). Copies are
+ * issued in slices of `slice_bytes` (0: library default, 4 MiB), each slice
+ * no earlier than its paced time, striped over `engines_per_ring` SDMA
+ * engines (0: library default). */
+typedef struct compass_links {
+    double fwd_Bps;
+    double bwd_Bps;
+    size_t slice_bytes;
+    int    engines_per_ring;
+} compass_links;
+
+/* ---- one operator instance ----------------------------------------------
+ * Describes the rank-local share of one AllGather+GEMM or GEMM+ReduceScatter.
+ * The emulated rank r owns row chunk r, rows [r*M/n, (r+1)*M/n).
+ *
+ * Requirements: 1 <= n <= 32, 0 <= rank < n, M % n == 0 (and M % (2n) == 0
+ * for the double ring), K % 8 == 0, N % 8 == 0, M*K*2, N*K*2 and M*N*4 below
+ * 2^31 bytes, M / 256 rounded up at most 512.
+ *
+ * AllGather + GEMM (pattern COMPASS_AG_GEMM):
+ *   shard_src[q], q = 0..n-1: (M/n) x K bf16 shard of rank q. shard_src[rank]
+ *     is device memory; if it is not already the rank's rows of `gathered`
+ *     it is copied there (on the stream) before the operator starts. The
+ *     others are device memory or pinned host memory; they are read by copy
+ *     engines only.
+ *   gathered: device, M x K bf16, receives every shard at its row chunk.
+ *   W: device, N x K bf16.  C: device, M x N bf16 output, C = gathered * W^T.
+ *
+ * GEMM + ReduceScatter (pattern COMPASS_GEMM_RS):
+ *   A: device, M x K bf16 (this rank's full input); W: device, N x K bf16.
+ *   partial_src[c], c = 0..n-1: (M/n) x N fp32 incoming partial sum of row
+ *     chunk c (device or pinned host). The partial of the rank's first
+ *     ReduceScatter step (a true ring has none there) is treated as resident:
+ *     unless partial_src of that chunk already points at its rows of
+ *     partial_stage, it is copied there (on the stream) before the operator
+ *     starts. The other n-1 arrive over the emulated link in ring order.
+ *   partial_stage: device, M x N fp32 landing buffer (chunk c at its rows).
+ *   C: device, M x N bf16: row chunk c = bf16(A[chunk c] * W^T + partial c).
+ *   send_dst: NULL, or n pointers; for every chunk c != rank, send_dst[c]
+ *     (device or pinned host, (M/n) x N bf16) receives chunk c of C as soon
+ *     as all of its tiles are stored — the emulated send to the next rank.
+ *
+ * Unused fields of the other pattern may be NULL. */
+typedef struct compass_problem {
+    int pattern;
+    int M, N, K;
+    int n, rank, ring;
+    const void *W;
+    void *C;
+    /* AllGather + GEMM */
+    const void *const *shard_src;
+    void *gathered;
+    /* GEMM + ReduceScatter */
+    const void *A;
+    const float *const *partial_src;
+    float *partial_stage;
+    void *const *send_dst;
+} compass_problem;
+
+/* ---- TA-IntraFusion: fused AllGather + GEMM (Section III-B, Fig. 6) ------
+ * One persistent bf16 MFMA GEMM kernel takes output tiles in ring-arrival
+ * order (compass_schedule) and waits on each partition's arrival flag before
+ * reading its rows; copy engines deliver the remote shards at the link
+ * rates. Returns once everything is enqueued; the kernel ends after every
+ * partition arrived and every tile is stored. */
+int compass_ag_gemm(const compass_problem *p, const compass_links *links, void *stream);
+
+/* ---- TA-IntraFusion: fused GEMM + ReduceScatter (Section III-B) ----------
+ * Tiles run in ReduceScatter order (local chunk last). The main loop never
+ * waits; the epilogue of a tile waits for its chunk's incoming partial, adds
+ * it in fp32 and stores bf16. When the last tile of a non-local chunk is
+ * stored, that chunk is sent to send_dst. A final wait on the stream covers
+ * the sends. */
+int compass_gemm_rs(const compass_problem *p, const compass_links *links, void *stream);
+
+/* ---- ODP-InterDecom with degree d (Section II-B Fig. 2(c); Section IV) ---
+ * d sub-operators: sub-operator j owns row piece j, rows
+ * [j*M/(n d), (j+1)*M/(n d)) of every chunk. AllGather: its pieces are
+ * gathered over the ring (ring order, paced), then a GEMM over those M/d
+ * rows writes them at their global positions; the copy engines run ahead,
+ * so gathering piece j+1 overlaps GEMM j. ReduceScatter: sub-GEMM j's
+ * epilogue waits for piece j of each chunk's partial. d must be a power of
+ * two dividing M/n (M/(2n) for the double ring); d = 1 is the sequential
+ * operator. */
+int compass_decomp_gemm(const compass_problem *p, int d, const compass_links *links, void *stream);
+
+/* ---- measurement companions ----------------------------------------------
+ * compass_gemm: the same GEMM kernel with nothing to wait for (T_gemm).
+ *   A: device M x K bf16, W: device N x K bf16, C: device M x N bf16,
+ *   P: NULL or device M x N fp32 added before rounding.
+ * compass_transfer: exactly the copies the fused operator of `p` issues, at
+ *   the same pacing, with no GEMM (T_xfer); a one-workgroup kernel on the
+ *   stream starts the copies and ends when the last one landed.
+ * compass_sequential: the unfused operator (T_unfused). AllGather: all
+ *   copies, then the GEMM (identical to compass_decomp_gemm with d = 1).
+ *   ReduceScatter: the GEMM first (its epilogue reads partial_stage as it is
+ *   at launch), then the incoming and outgoing copies. */
+int compass_gemm(int M, int N, int K, const void *A, const void *W, void *C,
+                 const float *P, void *stream);
+int compass_transfer(const compass_problem *p, const compass_links *links, void *stream);
+int compass_sequential(const compass_problem *p, const compass_links *links, void *stream);
+
+/* Wait until the copy side of every enqueued operator has finished and the
+ * device is idle; return the pending asynchronous status (COMPASS_OK or
+ * COMPASS_ERR_TIMEOUT) and clear it. */
+int compass_sync(void);
+
+/* ---- tuning / test options -------------------------------------------- */
+#define COMPASS_OPT_SPIN_LIMIT   1  /* max polls of one kernel-side wait (default ~2 s) */
+#define COMPASS_OPT_HOST_TIMEOUT 2  /* host-side wait bound, microseconds (default 5 s) */
+#define COMPASS_OPT_GRID         3  /* persistent grid size; 0 = one workgroup per CU */
+#define COMPASS_OPT_DROP_FLAG    4  /* test only: index of an AllGather partition whose
+                                       copy and flag are never issued; -1 = none */
+int compass_set_option(int key, long long value);
+
+/* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */
+typedef struct compass_workload {   /* W of Eq. 1 / Eq. 6 */
+    int pattern;                    /* COMPASS_AG_GEMM or COMPASS_GEMM_RS     */
+    int M, N, K, n;
+} compass_workload;
+
+typedef struct compass_topology {   /* T of Eq. 1 / Eq. 6 */
+    int    ring;                    /* COMPASS_RING_SINGLE / _DOUBLE          */
+    double fwd_Bps, bwd_Bps;        /* per-direction link rates, bytes/s      */
+    double step_latency_s;          /* fixed cost of one ring step            */
+} compass_topology;
+
+typedef struct compass_calib {
+    double comp_a, comp_b;          /* T_comp = comp_a + comp_b * 2MNK        */
+    double alpha_decomp, beta_decomp; /* Eq. 3 */
+    double alpha_fusion, beta_fusion; /* Eq. 8 */
+    int    d_max;                   /* largest degree considered (Table IV: 16) */
+    int    literal_eq5;             /* 1: Eq. 5 exactly as printed (1/lambda);
+                                       0: min(lambda, 1/lambda), the minimiser
+                                       in both the compute- and the
+                                       communication-bound regime            */
+} compass_calib;
+
+typedef struct compass_choice {     /* (S*, T*) of Algorithm 1, with details  */
+    int    strategy;                /* COMPASS_INTRA_FUSION / _INTER_DECOM    */
+    int    d_star, d_cand;          /* Eq. 4 and Eq. 5                        */
+    double t_star;                  /* min(T_fusion, T_decomp(d*))            */
+    double lambda;                  /* T_comp / T_comm                        */
+    double t_comp, t_comm;
+    double t_fusion;                /* Eq. 7 + Eq. 8                          */
+    double t_decomp;                /* Eq. 2 at d*                            */
+    double t_decomp1;               /* Eq. 2 at d = 1 (T_comp + T_comm)       */
+} compass_choice;
+
+/* Algorithm 1. T_comp is linear in 2MNK; T_comm is n-1 ring steps, each the
+ * slowest active ring's per-link bytes over its rate plus step_latency_s
+ * (AllGather moves the M x K bf16 input; ReduceScatter receives M x N fp32
+ * partials and sends M x N bf16 sums on the opposite link direction).
+ * d* is additionally limited to powers of two that split every chunk (double
+ * ring: every half-chunk) evenly. Host only, O(1); needs no GPU. */
+int compass_pick_strategy(const compass_workload *w, const compass_topology *t,
+                          const compass_calib *cal, compass_choice *out);
+
+/* Eq. 2 and Eq. 7-8 evaluated directly (host only). */
+double compass_model_t_decomp(double t_comp, double t_comm, int d, double alpha, double beta);
+double compass_model_t_fusion(const compass_workload *w, double t_comp, double t_comm_step,
+                              double alpha_f, double beta_f);
+
+/* ---- calibration (Section IV-C: offline linear regression) --------------
+ * Each sample is one measurement:
+ *   kind 0  GEMM alone:        t_meas of the plain GEMM on workload w
+ *   kind 1  InterDecom:        t_meas at degree d, with t_comp / t_comm the
+ *                              measured GEMM-alone and transfer-alone times
+ *   kind 2  IntraFusion:       t_meas of the fused operator, with t_comp /
+ *                              t_comm as above (t_comm = all n-1 steps)
+ * compass_calibrate fits comp_a/comp_b by least squares over kind-0 samples,
+ * alpha/beta_decomp over the per-sample overhead factors implied by Eq. 2
+ * (kind 1, d >= 2), and alpha/beta_fusion over the per-synchronisation
+ * overheads implied by Eq. 7 against Eq. 8's volume m (kind 2). Fields with
+ * fewer than two distinct abscissae stay as passed in. Host only. */
+typedef struct compass_sample {
+    int kind;
+    compass_workload w;
+    int d;
+    double t_meas, t_comp, t_comm;
+} compass_sample;
+int compass_calibrate(const compass_sample *s, int count, compass_calib *inout);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *compass_last_error(void);
+
+/* Library version string. */
+const char *compass_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* COMPASS_H */

@@ -1,0 +1,62 @@
+// extern "C" entry points declared in compass.h.
+#include "compass.h"
+#include "internal.h"
+
+using namespace compass;
+
+extern "C" {
+
+int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int cap) {
+    return schedule_fill(pattern, ring, n, rank, out, cap);
+}
+
+int compass_ag_gemm(const compass_problem *p, const compass_links *links, void *stream) {
+    return op_ag_gemm(p, links, stream);
+}
+
+int compass_gemm_rs(const compass_problem *p, const compass_links *links, void *stream) {
+    return op_gemm_rs(p, links, stream);
+}
+
+int compass_decomp_gemm(const compass_problem *p, int d, const compass_links *links, void *stream) {
+    return op_decomp(p, d, links, stream);
+}
+
+int compass_gemm(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream) {
+    return op_gemm(M, N, K, A, W, C, P, stream);
+}
+
+int compass_transfer(const compass_problem *p, const compass_links *links, void *stream) {
+    return op_transfer(p, links, stream);
+}
+
+int compass_sequential(const compass_problem *p, const compass_links *links, void *stream) {
+    return op_sequential(p, links, stream);
+}
+
+int compass_sync(void) { return op_sync(); }
+
+int compass_set_option(int key, long long value) { return op_set_option(key, value); }
+
+int compass_pick_strategy(const compass_workload *w, const compass_topology *t, const compass_calib *cal,
+                          compass_choice *out) {
+    return pick(w, t, cal, out);
+}
+
+double compass_model_t_decomp(double t_comp, double t_comm, int d, double alpha, double beta) {
+    return model_t_decomp(t_comp, t_comm, d, alpha, beta);
+}
+
+double compass_model_t_fusion(const compass_workload *w, double t_comp, double t_comm_step, double alpha_f,
+                              double beta_f) {
+    if (!w || w->n < 1) return -1.0;
+    return model_t_fusion(*w, t_comp, t_comm_step, alpha_f, beta_f);
+}
+
+int compass_calibrate(const compass_sample *s, int count, compass_calib *inout) { return calibrate(s, count, inout); }
+
+const char *compass_last_error(void) { return last_error(); }
+
+const char *compass_version(void) { return "compass-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

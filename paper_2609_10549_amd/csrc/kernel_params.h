@@ -1,0 +1,69 @@
+// Launch parameters shared by the host runtime and the gfx950 kernels.
+#pragma once
+#include <stdint.h>
+
+namespace compass {
+
+constexpr int kTileM = 256;          // output tile rows (M)
+constexpr int kTileN = 256;          // output tile columns (N)
+constexpr int kTileK = 64;           // K depth of one LDS stage
+constexpr int kThreads = 256;        // 4 waves of 64
+constexpr int kMaxRowTiles = 256;    // M up to 65536 rows per launch
+constexpr int kMaxParts = 64;        // partitions per launch (2 n, n <= 32)
+constexpr int kMaxFlags = 2048;      // arrival / done flag slots
+constexpr int kFinalFlag0 = kMaxFlags - 8;  // end-of-job flags
+constexpr int kMaxJoin = 80;
+
+// Where a tile waits for its partitions' arrival flags.
+enum GateMode : int {
+    kGateNone = 0,       // everything resident
+    kGateMain = 1,       // before the first A load (AllGather)
+    kGateEpilogue = 2,   // before adding the incoming partial (ReduceScatter)
+};
+
+struct GemmParams {
+    const uint16_t *A;   // bf16, rows addressed through the row map below
+    const uint16_t *W;   // bf16, N x K
+    uint16_t *C;         // bf16 output, rows addressed through the row map
+    const float *P;      // fp32 partial added before rounding (or null)
+    uint32_t a_bytes;    // extent of A in bytes (buffer bound)
+    uint32_t w_bytes;    // extent of W in bytes
+    int M, N, K;         // logical rows of this launch, columns, depth
+    int lda, ldw, ldc, ldp;
+    int tiles_m, tiles_n;
+    // logical row i -> physical row (i / piece) * pstride + poff + i % piece;
+    // piece == 0 means the identity map
+    int piece, pstride, poff;
+    // gating: flag index of partition p is flag_base + p
+    uint32_t *flags;         // arrival flags (fine-grained device memory)
+    int gate;                // GateMode
+    int flag_base;
+    int nparts;              // partitions used by this launch
+    uint64_t resident_mask;  // partitions present before the launch (no wait)
+    uint64_t send_mask;      // partitions whose completion is signalled
+    uint32_t epoch;
+    uint32_t spin_limit;
+    // ReduceScatter chunk-done tracking (done_host null: off)
+    uint32_t *done_cnt;      // device counters, indexed like flags
+    uint32_t *done_host;     // host-visible done flags, indexed like flags
+    // control
+    uint32_t *ctrl;          // [0] tile ticket, [1] exit counter
+    uint32_t *start_word;    // host-visible; written with epoch at start (or null)
+    uint32_t *err_word;      // host-visible error word
+    int grid;
+    uint16_t rt_order[kMaxRowTiles];   // processing order of the row tiles
+    uint64_t rt_touch[kMaxRowTiles];   // partitions each row tile depends on
+    uint32_t done_expect[kMaxParts];   // tiles per partition to count (0: none)
+};
+
+struct JoinParams {
+    uint32_t *flags;
+    uint32_t *start_word;   // written with epoch first (or null)
+    uint32_t *err_word;
+    uint32_t epoch;
+    uint32_t spin_limit;
+    int count;
+    uint16_t idx[kMaxJoin];
+};
+
+}  // namespace compass

@@ -1,0 +1,362 @@
+// gfx950 kernels of the Compass hot path.
+//
+// gemm_kernel: persistent bf16 GEMM, C = A * W^T with fp32 accumulation on
+// the CDNA4 matrix cores (v_mfma_f32_32x32x16_bf16) and one bf16
+// round-to-nearest-even store. Workgroups take 256 x 256 output tiles from an
+// atomic ticket counter in the order the host chose (ring-arrival order for
+// TA-IntraFusion, Section III-B), and, depending on the gate mode, wait on the
+// per-partition arrival flags published by the copy engines before reading A
+// (AllGather) or before adding the incoming partial sum (ReduceScatter).
+//
+// Data path per 256 x 256 tile: A and W stream through LDS in K-steps of 64,
+// double buffered; global -> LDS moves use buffer_load ... lds (no register
+// staging; out-of-range rows or K columns read as zero through the buffer
+// bound). Each of the 4 waves owns a 128 x 128 quadrant: 4 x 4 MFMA blocks of
+// 32 x 32, 256 fp32 accumulators per lane. LDS rows are 128 bytes; the 16-byte
+// chunks of row r are XOR-permuted with (r >> 1) & 7 so that a fragment read
+// (32 rows, one chunk) hits distinct banks.
+//
+// join_kernel: one wave that (optionally) marks the start of a transfer job
+// and waits for a list of flags, putting the end of the copy side onto the
+// stream.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernel_params.h"
+
+namespace compass {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define LDS_AS(p) ((__attribute__((address_space(3))) void *)(p))
+
+constexpr uint32_t kOOB = 0x80000000u;   // byte offset beyond every buffer bound
+constexpr int kWaveM = 128, kWaveN = 128;
+constexpr int kFragM = kWaveM / 32, kFragN = kWaveN / 32;
+constexpr int kStageBytes = kTileM * kTileK * 2;     // 32 KiB per operand
+constexpr int kLoadsPerWave = kStageBytes / 1024 / 4;  // 1 KiB per instruction
+
+static_assert(kTileM == kTileN, "loader assumes square tiles");
+
+__device__ __forceinline__ uint32_t ld_flag(const uint32_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Thread-0 wait for every partition in `mask`; system-scope acquire after.
+__device__ bool wait_flags(const uint32_t *flags, uint64_t mask, uint32_t epoch,
+                           uint32_t limit, uint32_t *err) {
+    while (mask) {
+        const int p = __builtin_ctzll(mask);
+        uint32_t polls = 0;
+        while ((int32_t)(ld_flag(&flags[p]) - epoch) < 0) {
+            if (++polls > limit) {
+                __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                return false;
+            }
+            if ((polls & 255u) == 0 && ld_flag(err) != 0) return false;
+            __builtin_amdgcn_s_sleep(4);
+        }
+        mask &= mask - 1;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+    return true;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const __bf16 a = (__bf16)lo, b = (__bf16)hi;   // round to nearest even
+    return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+__device__ __forceinline__ int map_row(const GemmParams &p, int i) {
+    if (p.piece == 0) return i;
+    const int q = i / p.piece;
+    return q * p.pstride + p.poff + (i - q * p.piece);
+}
+
+// Issue one K-stage (64 columns) of a 256-row operand into LDS. Load q of a
+// wave fills LDS bytes [(4q + wave) KiB, +1 KiB): rows 32q + 8 wave + lane/8,
+// physical chunk lane % 8, which holds logical chunk `cchunk` (the XOR
+// permutation; one value per lane). `row_off` is each load's row start in
+// bytes, kOOB past the last row.
+__device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rsrc, char *lds, const uint32_t *row_off,
+                                           int cchunk, int k0, int K, int wave) {
+    const int kc = k0 + cchunk * 8;
+    const bool kin = kc < K;
+#pragma unroll
+    for (int q = 0; q < kLoadsPerWave; ++q) {
+        const uint32_t off = (row_off[q] == kOOB || !kin) ? kOOB : row_off[q] + (uint32_t)kc * 2u;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_AS(lds + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
+    }
+}
+
+__device__ __forceinline__ void mma_stage(const char *sA, const char *sW, int lane, int wm0, int wn0,
+                                          f32x16 (&acc)[kFragN][kFragM]) {
+    const int r = lane & 31;
+    const int swz = (r >> 1) & 7;
+#pragma unroll
+    for (int kk = 0; kk < kTileK / 16; ++kk) {
+        const int c = 2 * kk + (lane >> 5);
+        const int coff = (c ^ swz) << 4;
+        bf16x8 a[kFragM], b[kFragN];
+#pragma unroll
+        for (int mi = 0; mi < kFragM; ++mi)
+            a[mi] = *reinterpret_cast<const bf16x8 *>(sA + (wm0 + mi * 32 + r) * 128 + coff);
+#pragma unroll
+        for (int ni = 0; ni < kFragN; ++ni)
+            b[ni] = *reinterpret_cast<const bf16x8 *>(sW + (wn0 + ni * 32 + r) * 128 + coff);
+#pragma unroll
+        for (int ni = 0; ni < kFragN; ++ni)
+#pragma unroll
+            for (int mi = 0; mi < kFragM; ++mi)
+                acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ni], a[mi], acc[ni][mi], 0, 0, 0);
+    }
+}
+
+// RS = false: optional main-loop gate (AllGather), plain store.
+// RS = true: optional epilogue gate, fp32 partial add, chunk-done signalling.
+template <bool RS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_kernel(const GemmParams p) {
+    __shared__ __attribute__((aligned(1024))) char sA0[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) char sA1[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) char sW0[kStageBytes];
+    __shared__ __attribute__((aligned(1024))) char sW1[kStageBytes];
+    __shared__ uint32_t s_ticket;
+    __shared__ int s_ok;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm0 = (wave >> 1) * kWaveM;
+    const int wn0 = (wave & 1) * kWaveN;
+    const int total = p.tiles_m * p.tiles_n;
+    const int KT2 = (((p.K + kTileK - 1) / kTileK) + 1) & ~1;
+
+    const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, (int)p.w_bytes, 0x00020000);
+
+    // loader geometry: row of load q is 32 q + lrow0; logical chunk of the lane
+    const int lrow0 = 8 * wave + (lane >> 3);
+    const int cchunk = (lane & 7) ^ ((4 * wave + (lane >> 4)) & 7);
+
+    uint64_t known = 0;   // partitions already acquired by this workgroup
+    bool failed = false;
+
+    if (tid == 0) {
+        const uint32_t t = __hip_atomic_fetch_add(&p.ctrl[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (t == 0 && p.start_word)
+            __hip_atomic_store(p.start_word, p.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        s_ticket = t;
+    }
+    __syncthreads();
+    uint32_t ticket = s_ticket;
+
+    while ((int)ticket < total) {
+        const int ti = (int)ticket / p.tiles_n;
+        const int tn = (int)ticket - ti * p.tiles_n;
+        const int rt = p.rt_order[ti];
+        const int m0 = rt * kTileM;
+        const int n0 = tn * kTileN;
+        const uint64_t touch = p.rt_touch[rt];
+        const uint64_t need = touch & ~p.resident_mask & ~known;
+
+        if (!RS && p.gate == kGateMain && need) {
+            if (tid == 0) s_ok = wait_flags(p.flags + p.flag_base, need, p.epoch, p.spin_limit, p.err_word);
+            __syncthreads();
+            if (!s_ok) failed = true;
+            known |= need;
+        }
+
+        f32x16 acc[kFragN][kFragM];
+#pragma unroll
+        for (int ni = 0; ni < kFragN; ++ni)
+#pragma unroll
+            for (int mi = 0; mi < kFragM; ++mi)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[ni][mi][e] = 0.0f;
+
+        {   // a timed-out tile still runs (its loads stay in bounds); only its
+            // stores are dropped
+            uint32_t offA[kLoadsPerWave], offW[kLoadsPerWave];
+#pragma unroll
+            for (int q = 0; q < kLoadsPerWave; ++q) {
+                const int ia = m0 + 32 * q + lrow0;
+                offA[q] = ia < p.M ? (uint32_t)map_row(p, ia) * (uint32_t)p.lda * 2u : kOOB;
+                const int iw = n0 + 32 * q + lrow0;
+                offW[q] = iw < p.N ? (uint32_t)iw * (uint32_t)p.ldw * 2u : kOOB;
+            }
+            load_stage(rA, sA0, offA, cchunk, 0, p.K, wave);
+            load_stage(rW, sW0, offW, cchunk, 0, p.K, wave);
+            // An even number of K-steps keeps the loop free of early exits (the
+            // accumulators then stay in place); a padding step reads only
+            // out-of-range columns, i.e. zeros.
+            for (int kt = 0; kt < KT2; kt += 2) {
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+                load_stage(rA, sA1, offA, cchunk, (kt + 1) * kTileK, p.K, wave);
+                load_stage(rW, sW1, offW, cchunk, (kt + 1) * kTileK, p.K, wave);
+                mma_stage(sA0, sW0, lane, wm0, wn0, acc);
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+                if (kt + 2 < KT2) {
+                    load_stage(rA, sA0, offA, cchunk, (kt + 2) * kTileK, p.K, wave);
+                    load_stage(rW, sW0, offW, cchunk, (kt + 2) * kTileK, p.K, wave);
+                }
+                mma_stage(sA1, sW1, lane, wm0, wn0, acc);
+            }
+        }
+
+        // fetch the next ticket while the epilogue runs
+        if (tid == 0)
+            s_ticket = __hip_atomic_fetch_add(&p.ctrl[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+        if (RS && p.gate == kGateEpilogue && need) {
+            if (tid == 0) s_ok = failed ? 0 : wait_flags(p.flags + p.flag_base, need, p.epoch, p.spin_limit, p.err_word);
+            __syncthreads();
+            if (!s_ok) failed = true;
+            known |= need;
+        }
+
+        if (!RS) {
+            const int r = lane & 31;
+            const int hi = lane >> 5;
+            const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
+#pragma unroll
+            for (int mi = 0; mi < kFragM; ++mi) {
+                const int m = m0 + wm0 + mi * 32 + r;
+                if (m >= mlim) continue;
+                uint16_t *crow = p.C + (size_t)map_row(p, m) * p.ldc;
+#pragma unroll
+                for (int ni = 0; ni < kFragN; ++ni) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int n = n0 + wn0 + ni * 32 + 8 * g + 4 * hi;
+                        if (n >= p.N) continue;
+                        uint2 o;
+                        o.x = pack_bf16x2(acc[ni][mi][4 * g + 0], acc[ni][mi][4 * g + 1]);
+                        o.y = pack_bf16x2(acc[ni][mi][4 * g + 2], acc[ni][mi][4 * g + 3]);
+                        *reinterpret_cast<uint2 *>(crow + n) = o;
+                    }
+                }
+            }
+        } else {
+            // Each 32 x 32 fp32 block goes through a per-wave 4 KiB LDS patch
+            // (rows of 128 bytes, 16-byte chunks XOR-permuted by row & 7) and
+            // comes back row-contiguous: 8 lanes per row add 128 contiguous
+            // bytes of the partial sum and store 64 contiguous bytes of C.
+            char *patch = sA0 + wave * 4096;
+            const int r = lane & 31;
+            const int hi = lane >> 5;
+            const int rr = lane >> 3;          // read-back row within 8
+            const int rc = lane & 7;           // read-back chunk (4 floats)
+            const int mlim = failed ? 0 : p.M;
+#pragma unroll
+            for (int mi = 0; mi < kFragM; ++mi) {
+#pragma unroll
+                for (int ni = 0; ni < kFragN; ++ni) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int cc = 2 * g + hi;
+                        f32x4 v = {acc[ni][mi][4 * g + 0], acc[ni][mi][4 * g + 1],
+                                   acc[ni][mi][4 * g + 2], acc[ni][mi][4 * g + 3]};
+                        *reinterpret_cast<f32x4 *>(patch + r * 128 + ((cc ^ (r & 7)) << 4)) = v;
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): patch written
+#pragma unroll
+                    for (int it = 0; it < 4; ++it) {
+                        const int row = rr + 8 * it;
+                        const f32x4 v = *reinterpret_cast<const f32x4 *>(patch + row * 128 + ((rc ^ (row & 7)) << 4));
+                        const int m = m0 + wm0 + mi * 32 + row;
+                        const int n = n0 + wn0 + ni * 32 + 4 * rc;
+                        if (m < mlim && n < p.N) {
+                            const int pm = map_row(p, m);
+                            float v0 = v[0], v1 = v[1], v2 = v[2], v3 = v[3];
+                            if (p.P) {
+                                const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
+                                v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
+                            }
+                            uint2 o;
+                            o.x = pack_bf16x2(v0, v1);
+                            o.y = pack_bf16x2(v2, v3);
+                            *reinterpret_cast<uint2 *>(p.C + (size_t)pm * p.ldc + n) = o;
+                        }
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // patch read before reuse
+                }
+            }
+        }
+
+        __syncthreads();   // stores issued and complete; LDS free for the next tile
+        if (RS && p.done_host && !failed && tid == 0) {
+            uint64_t dm = touch & p.send_mask;
+            if (dm) {
+                __threadfence_system();   // tile data written back before counting
+                while (dm) {
+                    const int q = __builtin_ctzll(dm);
+                    const uint32_t old = __hip_atomic_fetch_add(&p.done_cnt[p.flag_base + q], 1u,
+                                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (old + 1u == p.done_expect[q])
+                        __hip_atomic_store(&p.done_host[p.flag_base + q], p.epoch, __ATOMIC_RELEASE,
+                                           __HIP_MEMORY_SCOPE_SYSTEM);
+                    dm &= dm - 1;
+                }
+            }
+        }
+        ticket = s_ticket;
+    }
+
+    // exit: the last workgroup out resets the shared counters
+    __syncthreads();
+    if (tid == 0) {
+        const uint32_t old = __hip_atomic_fetch_add(&p.ctrl[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == (uint32_t)p.grid - 1u) {
+            if (RS && p.done_host)
+                for (int q = 0; q < p.nparts; ++q)
+                    __hip_atomic_store(&p.done_cnt[p.flag_base + q], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&p.ctrl[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&p.ctrl[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
+template __global__ void gemm_kernel<false>(const GemmParams);
+template __global__ void gemm_kernel<true>(const GemmParams);
+
+__global__ __launch_bounds__(64) void join_kernel(const JoinParams j) {
+    if (threadIdx.x != 0) return;
+    if (j.start_word) __hip_atomic_store(j.start_word, j.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    for (int i = 0; i < j.count; ++i) {
+        const uint32_t *f = j.flags + j.idx[i];
+        uint32_t polls = 0;
+        while ((int32_t)(ld_flag(f) - j.epoch) < 0) {
+            if (++polls > j.spin_limit) {
+                __hip_atomic_fetch_or(j.err_word, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                return;
+            }
+            if ((polls & 255u) == 0 && ld_flag(j.err_word) != 0) return;
+            __builtin_amdgcn_s_sleep(8);
+        }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
+}
+
+}  // namespace compass
+
+namespace compass {
+
+hipError_t launch_gemm(const GemmParams &p, bool rs, hipStream_t stream) {
+    if (rs)
+        hipLaunchKernelGGL(gemm_kernel<true>, dim3(p.grid), dim3(kThreads), 0, stream, p);
+    else
+        hipLaunchKernelGGL(gemm_kernel<false>, dim3(p.grid), dim3(kThreads), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_join(const JoinParams &j, hipStream_t stream) {
+    hipLaunchKernelGGL(join_kernel, dim3(1), dim3(64), 0, stream, j);
+    return hipGetLastError();
+}
+
+}  // namespace compass

@@ -1,0 +1,218 @@
+// Host-side parts of the Compass hot path that need no GPU: ring schedules
+// (Section III-A/B), the InterDecom and IntraFusion time models (Eq. 2-8),
+// the strategy selector (Algorithm 1) and the calibration fits
+// (Section IV-C). Everything is fp64 and O(1) per call.
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "compass.h"
+#include "internal.h"
+
+namespace compass {
+
+int schedule_fill(int pattern, int ring, int n, int rank, int32_t *out, int cap) {
+    if (n < 1 || n > kMaxRanks || rank < 0 || rank >= n)
+        return set_error(COMPASS_ERR_INVALID, "schedule: need 1 <= n <= 32 and 0 <= rank < n");
+    if (pattern != COMPASS_AG_GEMM && pattern != COMPASS_GEMM_RS)
+        return set_error(COMPASS_ERR_INVALID, "schedule: unknown pattern");
+    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE)
+        return set_error(COMPASS_ERR_INVALID, "schedule: unknown ring");
+    const int len = ring == COMPASS_RING_SINGLE ? n : 2 * n;
+    if (!out || cap < len) return set_error(COMPASS_ERR_INVALID, "schedule: output too small");
+    auto md = [n](int x) { return ((x % n) + n) % n; };
+    int k = 0;
+    if (pattern == COMPASS_AG_GEMM) {
+        if (ring == COMPASS_RING_SINGLE) {
+            // step s holds the chunk that travelled s hops on the forward ring
+            for (int s = 0; s < n; ++s) out[k++] = md(rank - s);
+        } else {
+            out[k++] = 2 * rank;          // local halves first
+            out[k++] = 2 * rank + 1;
+            for (int s = 1; s < n; ++s) {
+                out[k++] = 2 * md(rank - s) + 1;  // odd half, forward ring
+                out[k++] = 2 * md(rank + s);      // even half, backward ring
+            }
+        }
+    } else {
+        if (ring == COMPASS_RING_SINGLE) {
+            for (int s = 0; s < n; ++s) out[k++] = md(rank - 1 - s);
+        } else {
+            for (int s = 0; s < n; ++s) {
+                out[k++] = 2 * md(rank - 1 - s) + 1;
+                out[k++] = 2 * md(rank + 1 + s);
+            }
+        }
+    }
+    return k;
+}
+
+// Bytes one ring link carries per step (incoming, outgoing). AllGather moves
+// the M x K bf16 input; ReduceScatter receives M x N fp32 partials and sends
+// M x N bf16 sums. A single ring moves m/n per step, the double ring m/(2n)
+// per ring (Section III-A).
+static void step_bytes(const compass_workload &w, int ring, double *in, double *out) {
+    const double div = ring == COMPASS_RING_SINGLE ? w.n : 2.0 * w.n;
+    if (w.pattern == COMPASS_AG_GEMM) {
+        *in = (double)w.M * w.K * 2.0 / div;
+        *out = 0.0;
+    } else {
+        *in = (double)w.M * w.N * 4.0 / div;
+        *out = (double)w.M * w.N * 2.0 / div;
+    }
+}
+
+double model_t_comm(const compass_workload &w, const compass_topology &t) {
+    double in, out;
+    step_bytes(w, t.ring, &in, &out);
+    double step = 0.0;
+    const int rings = t.ring == COMPASS_RING_SINGLE ? 1 : 2;
+    for (int i = 0; i < rings; ++i) {
+        const double r = i == 0 ? t.fwd_Bps : t.bwd_Bps;
+        step = std::fmax(step, std::fmax(in / r, out / r));
+    }
+    return (w.n - 1) * (step + t.step_latency_s);
+}
+
+double model_t_comp(const compass_workload &w, const compass_calib &c) {
+    return c.comp_a + c.comp_b * (2.0 * w.M * (double)w.N * w.K);
+}
+
+double model_t_decomp(double tc, double tm, int d, double alpha, double beta) {
+    // Eq. 2 with Eq. 3: (d-1) stages of max(Tc, Tm)/d scaled by eta(d), plus
+    // the non-overlapped Tc/d + Tm/d.
+    const double stage = std::fmax(tc / d, tm / d);
+    return (d - 1) * stage * (alpha + beta * d) + tc / d + tm / d;
+}
+
+int p2_round(double x) {
+    // nearest power of two in log2; ties to the smaller power; < 1 -> 1
+    if (!(x > 1.0)) return 1;
+    const double lg = std::log2(x);
+    const double k = std::floor(lg);
+    const double frac = lg - k;
+    const int e = (int)k + (frac > 0.5 ? 1 : 0);
+    if (e >= 30) return 1 << 30;
+    return 1 << e;
+}
+
+double d_stationary(double lam, double alpha, double beta, int literal) {
+    if (beta <= 0.0) return INFINITY;
+    const double r = literal ? 1.0 / lam : std::fmin(lam, 1.0 / lam);
+    const double num = 1.0 - alpha + r;
+    if (num <= 0.0) return 0.0;
+    return std::sqrt(num / beta);
+}
+
+double model_t_fusion(const compass_workload &w, double tc, double tm_step, double af, double bf) {
+    // Eq. 7: chunk 1 exposes its computation; chunks 2..n overlap their
+    // computation (Tc/n each) with one ring step of communication; Eq. 8 adds
+    // n-1 synchronisation overheads alpha_f + beta_f * m.
+    const int n = w.n;
+    const double c = tc / n;
+    double body = 0.0;
+    for (int i = 1; i < n; ++i) body += std::fmax(c, tm_step);
+    const double m = w.pattern == COMPASS_AG_GEMM ? (double)w.M * w.K : (double)w.M * w.N;
+    return body + c + (n - 1) * (af + bf * m);
+}
+
+int pick(const compass_workload *w, const compass_topology *t, const compass_calib *cal,
+         compass_choice *out) {
+    if (!w || !t || !cal || !out) return set_error(COMPASS_ERR_INVALID, "pick_strategy: null argument");
+    if (w->n < 1 || w->M < 1 || w->N < 1 || w->K < 1 || w->M % w->n)
+        return set_error(COMPASS_ERR_INVALID, "pick_strategy: bad workload");
+    if (w->pattern != COMPASS_AG_GEMM && w->pattern != COMPASS_GEMM_RS)
+        return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown pattern");
+    if (t->ring != COMPASS_RING_SINGLE && t->ring != COMPASS_RING_DOUBLE)
+        return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown ring");
+    if (!(t->fwd_Bps > 0) || (t->ring == COMPASS_RING_DOUBLE && !(t->bwd_Bps > 0)))
+        return set_error(COMPASS_ERR_INVALID, "pick_strategy: link rates must be positive");
+    if (cal->d_max < 1) return set_error(COMPASS_ERR_INVALID, "pick_strategy: d_max < 1");
+    // Phase 1: base metrics
+    const double tc = model_t_comp(*w, *cal);
+    const double tm = model_t_comm(*w, *t);
+    if (!(tc > 0) || !(tm > 0)) return set_error(COMPASS_ERR_INVALID, "pick_strategy: non-positive base time");
+    const double lam = tc / tm;
+    // Phase 2: degree (Eq. 5 then Eq. 4), limited to even splits of a chunk
+    const int rows = w->M / w->n;
+    int feas = 1;
+    while (feas * 2 <= cal->d_max && rows % (feas * 2) == 0) feas *= 2;
+    const double x = d_stationary(lam, cal->alpha_decomp, cal->beta_decomp, cal->literal_eq5);
+    int dc = std::isinf(x) ? feas : p2_round(x);
+    if (dc > feas) dc = feas;
+    if (dc < 1) dc = 1;
+    const double t1 = model_t_decomp(tc, tm, 1, cal->alpha_decomp, cal->beta_decomp);
+    const double tdc = model_t_decomp(tc, tm, dc, cal->alpha_decomp, cal->beta_decomp);
+    const int dstar = tdc < t1 ? dc : 1;
+    const double tdec = dstar == dc ? tdc : t1;
+    // Phase 3: both predictions and the choice
+    const double step = w->n > 1 ? tm / (w->n - 1) : 0.0;
+    const double tfus = model_t_fusion(*w, tc, step, cal->alpha_fusion, cal->beta_fusion);
+    out->strategy = tfus < tdec ? COMPASS_INTRA_FUSION : COMPASS_INTER_DECOM;
+    out->t_star = std::fmin(tfus, tdec);
+    out->d_star = dstar;
+    out->d_cand = dc;
+    out->lambda = lam;
+    out->t_comp = tc;
+    out->t_comm = tm;
+    out->t_fusion = tfus;
+    out->t_decomp = tdec;
+    out->t_decomp1 = t1;
+    return COMPASS_OK;
+}
+
+// Least squares y ~ a + b x; false when fewer than two distinct x.
+static bool fit_line(const std::vector<double> &x, const std::vector<double> &y, double *a, double *b) {
+    const size_t n = x.size();
+    if (n < 2) return false;
+    double mx = 0, my = 0;
+    for (size_t i = 0; i < n; ++i) { mx += x[i]; my += y[i]; }
+    mx /= n; my /= n;
+    double sxx = 0, sxy = 0;
+    for (size_t i = 0; i < n; ++i) { sxx += (x[i] - mx) * (x[i] - mx); sxy += (x[i] - mx) * (y[i] - my); }
+    if (!(sxx > 0)) return false;
+    *b = sxy / sxx;
+    *a = my - *b * mx;
+    return true;
+}
+
+int calibrate(const compass_sample *s, int count, compass_calib *c) {
+    if (!c || count < 0 || (count > 0 && !s)) return set_error(COMPASS_ERR_INVALID, "calibrate: bad arguments");
+    std::vector<double> x0, y0, x1, y1, x2, y2;
+    for (int i = 0; i < count; ++i) {
+        const compass_sample &q = s[i];
+        if (q.w.n < 1) return set_error(COMPASS_ERR_INVALID, "calibrate: sample with n < 1");
+        if (q.kind == 0) {
+            x0.push_back(2.0 * q.w.M * (double)q.w.N * q.w.K);
+            y0.push_back(q.t_meas);
+        } else if (q.kind == 1) {
+            if (q.d < 2) continue;
+            // invert Eq. 2 for the overhead factor at this point
+            const double d = q.d;
+            const double e = (q.t_meas - (q.t_comp + q.t_comm) / d) * d /
+                             ((d - 1) * std::fmax(q.t_comp, q.t_comm));
+            x1.push_back(d);
+            y1.push_back(e);
+        } else if (q.kind == 2) {
+            if (q.w.n < 2) continue;
+            // invert Eq. 7 for the per-synchronisation overhead
+            const int n = q.w.n;
+            const double cc = q.t_comp / n, ms = q.t_comm / (n - 1);
+            double base = cc;
+            for (int k = 1; k < n; ++k) base += std::fmax(cc, ms);
+            const double o = (q.t_meas - base) / (n - 1);
+            const double m = q.w.pattern == COMPASS_AG_GEMM ? (double)q.w.M * q.w.K : (double)q.w.M * q.w.N;
+            x2.push_back(m);
+            y2.push_back(o);
+        } else {
+            return set_error(COMPASS_ERR_INVALID, "calibrate: unknown sample kind");
+        }
+    }
+    double a, b;
+    if (fit_line(x0, y0, &a, &b)) { c->comp_a = a; c->comp_b = b; }
+    if (fit_line(x1, y1, &a, &b)) { c->alpha_decomp = a; c->beta_decomp = b; }
+    if (fit_line(x2, y2, &a, &b)) { c->alpha_fusion = a; c->beta_fusion = b; }
+    return COMPASS_OK;
+}
+
+}  // namespace compass

@@ -1,0 +1,159 @@
+"""Host-only checks of the C ABI (no GPU): the library loads and exports every
+function declared in include/compass.h; the host calls (schedule, models,
+selector, calibration) agree with the oracle — integers exactly, times to
+1e-12 relative."""
+import ctypes
+import math
+import os
+import random
+import re
+
+import pytest
+
+import oracle as O
+from paper_2609_10549_amd import compass as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "compass.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(compass_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = C.lib()
+    names = declared_functions()
+    assert len(names) >= 14
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(C._SIGS), "binding and header disagree"
+
+
+def test_struct_sizes_match_c_layout():
+    assert ctypes.sizeof(C.compass_links) == 32
+    assert ctypes.sizeof(C.compass_problem) == 4 * 7 + 4 + 8 * 8
+    assert ctypes.sizeof(C.compass_calib) == 6 * 8 + 8
+    assert ctypes.sizeof(C.compass_choice) == 3 * 4 + 4 + 7 * 8
+
+
+@pytest.mark.parametrize("pattern", ["ag", "rs"])
+@pytest.mark.parametrize("ring", ["single", "double"])
+def test_schedule_bit_exact_vs_oracle(pattern, ring):
+    for n in [1, 2, 3, 4, 5, 8, 16, 32]:
+        for r in range(n):
+            assert C.compass_schedule(pattern, ring, n, r) == O.schedule(pattern, ring, n, r)
+
+
+def test_schedule_errors():
+    with pytest.raises(C.CompassError) as e:
+        C.compass_schedule("ag", "single", 4, 4)
+    assert e.value.code == C.ERR_INVALID
+    with pytest.raises(C.CompassError):
+        C.compass_schedule("ag", "single", 33, 0)
+    assert "rank" in C.compass_last_error()
+
+
+def _rel(a, b):
+    return abs(a - b) / max(abs(b), 1e-300)
+
+
+def test_model_functions_match_oracle():
+    rng = random.Random(1)
+    for _ in range(200):
+        Tc, Tm = rng.uniform(0.1, 10), rng.uniform(0.1, 10)
+        d = rng.choice([1, 2, 4, 8, 16])
+        a, b = rng.uniform(0.5, 1.5), rng.uniform(0, 0.3)
+        assert _rel(C.compass_model_t_decomp(Tc, Tm, d, a, b), O.t_decomp(Tc, Tm, d, a, b)) < 1e-12
+        n = rng.choice([2, 4, 8])
+        pat = rng.choice(["ag", "rs"])
+        M, N, K = 1024 * n, rng.choice([2048, 4096]), rng.choice([4096, 8192])
+        w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+        af, bf = rng.uniform(0, 1e-4), rng.uniform(0, 1e-12)
+        step = Tm / (n - 1)
+        ref = O.t_fusion([Tc / n] * n, [0.0] + [step] * (n - 1), af, bf, O.fusion_m(pat, M, N, K))
+        assert _rel(C.compass_model_t_fusion(w, Tc, step, af, bf), ref) < 1e-12
+
+
+def _pick_both(pat, ring, M, N, K, n, fwd, bwd, tau, cal):
+    w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+    t = C.compass_topology(ring=C.RINGS[ring], fwd_Bps=fwd, bwd_Bps=bwd, step_latency_s=tau)
+    c = C.compass_calib(**cal)
+    got = C.compass_pick_strategy(w, t, c)
+    ref = O.pick_strategy(pat, ring, M, N, K, n, fwd, bwd, tau, cal["comp_a"], cal["comp_b"],
+                          cal["alpha_decomp"], cal["beta_decomp"], cal["alpha_fusion"], cal["beta_fusion"],
+                          d_max=cal["d_max"], literal=bool(cal["literal_eq5"]))
+    return got, ref
+
+
+def test_pick_strategy_matches_oracle_over_table4():
+    rng = random.Random(4)
+    wl = O.table4_workloads()
+    strategies = set()
+    for i, (pat, M, N, K, n) in enumerate(wl):
+        ring = "double" if i % 2 else "single"
+        fwd = rng.uniform(5e9, 400e9)
+        bwd = fwd / rng.choice([1.0, 4.0])
+        cal = dict(comp_a=rng.uniform(0, 2e-5), comp_b=1.0 / rng.uniform(3e14, 2e15),
+                   alpha_decomp=rng.uniform(0.7, 1.2), beta_decomp=rng.uniform(0.0, 0.15),
+                   alpha_fusion=rng.uniform(0, 5e-5), beta_fusion=rng.uniform(0, 1e-13),
+                   d_max=16, literal_eq5=i % 3 == 0)
+        got, ref = _pick_both(pat, ring, M, N, K, n, fwd, bwd, rng.uniform(0, 2e-5), cal)
+        assert got.d_star == ref["d_star"] and got.d_cand == ref["d_cand"]
+        assert got.strategy == (C.INTRA_FUSION if ref["strategy"] == "intra_fusion" else C.INTER_DECOM)
+        for k, kk in [("t_comp", "t_comp"), ("t_comm", "t_comm"), ("lambda_", "lam"), ("t_fusion", "t_fusion"),
+                      ("t_decomp", "t_decomp"), ("t_decomp1", "t_decomp1"), ("t_star", "t_star")]:
+            assert _rel(getattr(got, k), ref[kk]) < 1e-12, k
+        strategies.add(got.strategy)
+    assert strategies == {C.INTRA_FUSION, C.INTER_DECOM}   # both branches exercised
+
+
+def test_pick_strategy_rejects_bad_inputs():
+    w = C.compass_workload(pattern=0, M=1001, N=64, K=64, n=8)   # M % n != 0
+    t = C.compass_topology(ring=0, fwd_Bps=1e9, bwd_Bps=1e9, step_latency_s=0)
+    c = C.compass_calib(comp_a=0, comp_b=1e-12, alpha_decomp=1, beta_decomp=0.1, d_max=16)
+    with pytest.raises(C.CompassError):
+        C.compass_pick_strategy(w, t, c)
+    w.M = 1024
+    t.fwd_Bps = 0
+    with pytest.raises(C.CompassError):
+        C.compass_pick_strategy(w, t, c)
+
+
+def test_calibrate_matches_oracle_fits():
+    rng = random.Random(8)
+    samples, xs0, ys0, xs1, ys1, xs2, ys2 = [], [], [], [], [], [], []
+    for i in range(30):
+        n = rng.choice([4, 8])
+        pat = rng.choice(["ag", "rs"])
+        M, N, K = 1024 * n, rng.choice([2048, 4096]), rng.choice([2048, 8192])
+        w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+        kind = i % 3
+        Tc, Tm = rng.uniform(1e-4, 1e-3), rng.uniform(1e-4, 1e-3)
+        d = rng.choice([2, 4, 8, 16])
+        t = rng.uniform(2e-4, 3e-3)
+        samples.append(C.compass_sample(kind=kind, w=w, d=d, t_meas=t, t_comp=Tc, t_comm=Tm))
+        if kind == 0:
+            xs0.append(2.0 * M * N * K)
+            ys0.append(t)
+        elif kind == 1:
+            xs1.append(d)
+            ys1.append(O.eta_observed(t, Tc, Tm, d))
+        else:
+            xs2.append(O.fusion_m(pat, M, N, K))
+            ys2.append(O.fusion_overhead_observed(t, [Tc / n] * n, [0.0] + [Tm / (n - 1)] * (n - 1)))
+    cal = C.compass_calibrate(samples, C.compass_calib(d_max=16))
+    a0, b0 = O.fit_line(xs0, ys0)
+    a1, b1 = O.fit_line(xs1, ys1)
+    a2, b2 = O.fit_line(xs2, ys2)
+    for got, ref in [(cal.comp_a, a0), (cal.comp_b, b0), (cal.alpha_decomp, a1), (cal.beta_decomp, b1),
+                     (cal.alpha_fusion, a2), (cal.beta_fusion, b2)]:
+        assert math.isclose(got, ref, rel_tol=1e-9, abs_tol=1e-18)
+
+
+def test_calibrate_keeps_fields_without_data():
+    cal = C.compass_calib(comp_a=1.0, comp_b=2.0, alpha_decomp=3.0, beta_decomp=4.0,
+                          alpha_fusion=5.0, beta_fusion=6.0, d_max=16)
+    C.compass_calibrate([], cal)
+    assert (cal.comp_a, cal.beta_fusion) == (1.0, 6.0)

@@ -1,0 +1,270 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Bars: bf16 outputs within 5e-3 normwise relative error; integer-valued inputs
+(every fp32 partial sum exact) bit-exact against the oracle's exact result
+rounded to bf16 (nearest-even); schedules and index work bit-exact."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+import oracle as O  # noqa: E402
+from paper_2609_10549_amd import compass as C  # noqa: E402
+from synth import make_ag_inputs, make_int_ag_inputs, make_int_rs_inputs, make_rs_inputs  # noqa: E402
+from tests.gpu_helpers import TOL, AGCase, RSCase, host_bits, host_f64, rel_err, dev_bits  # noqa: E402
+
+FAST = C.links(200e9, 200e9)   # emulated link rates for functional tests
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+@pytest.fixture(autouse=True)
+def _sync_after():
+    yield
+    C.compass_sync()
+
+
+# ------------------------------------------------------------ plain GEMM
+@pytest.mark.parametrize("M,N,K", [(256, 256, 64), (300, 264, 200), (777, 520, 1032), (64, 8, 8), (1, 16, 8)])
+def test_gemm_integer_exact(M, N, K):
+    _say("gemm int", M, N, K)
+    inp = make_int_ag_inputs(M, N, K, 1, seed=M + N + K)
+    A = dev_bits(inp["shards"][0])
+    W = dev_bits(inp["W"])
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    C.compass_gemm(A, W, Cm)
+    torch.cuda.synchronize()
+    ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
+    assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref))
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 1024, 512), (1000, 776, 4104)])
+def test_gemm_random(M, N, K):
+    _say("gemm rand", M, N, K)
+    inp = make_ag_inputs(M, N, K, 1, seed=5, dist_a=("normal", 1.0), dist_w=("normal", 0.02))
+    A = dev_bits(inp["shards"][0])
+    W = dev_bits(inp["W"])
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    C.compass_gemm(A, W, Cm)
+    torch.cuda.synchronize()
+    ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
+    assert rel_err(host_f64(Cm), ref) < TOL
+
+
+def test_gemm_with_partial_integer_exact():
+    M, N, K = 520, 264, 136
+    inp = make_int_rs_inputs(M, N, K, 1, seed=3)
+    A, W = dev_bits(inp["A"]), dev_bits(inp["W"])
+    P = torch.from_numpy(inp["P_in"][0]).cuda()
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    C.compass_gemm(A, W, Cm, P)
+    torch.cuda.synchronize()
+    ref = O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]), [inp["P_in"][0].astype(np.float64)], 1)
+    assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref))
+
+
+# ------------------------------------------------------------ fused AllGather+GEMM
+@pytest.mark.parametrize("ring", ["single", "double"])
+@pytest.mark.parametrize("n", [2, 4, 8])
+def test_ag_gemm_integer_exact_all_ranks(ring, n):
+    M, N, K = 64 * n * (2 if ring == "double" else 1) + 0, 264, 200
+    inp = make_int_ag_inputs(M, N, K, n, seed=10 + n)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    for r in range(n):
+        _say("ag int", ring, n, r, M, N, K)
+        case = AGCase(inp, r, ring)
+        C.compass_ag_gemm(case.problem, FAST)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+
+
+def test_ag_gemm_config1_all_ranks():
+    # AllGather-GEMM, TP=2: shards 256x512 U[-1,1], B 512x1024, single ring
+    inp = make_ag_inputs(512, 1024, 512, 2, seed=1, dist_a=("uniform", -1.0, 1.0), dist_w=("uniform", -1.0, 1.0))
+    for r in range(2):
+        _say("config1 rank", r)
+        case = AGCase(inp, r, "single")
+        C.compass_ag_gemm(case.problem, FAST)
+        C.compass_sync()
+        assert rel_err(host_f64(case.C), case.reference()) < TOL
+
+
+@pytest.mark.parametrize("ring", ["single", "double"])
+def test_ag_gemm_ragged_multi_tile_pinned_sources(ring):
+    # several row tiles per partition, a ragged N and K, remote shards in pinned host memory
+    n = 4
+    M, N, K = 2048, 776, 1032
+    inp = make_ag_inputs(M, N, K, n, seed=77)
+    case = AGCase(inp, 1, ring, pinned_remote=True, local_in_place=False)
+    _say("ag ragged pinned", ring)
+    C.compass_ag_gemm(case.problem, C.links(50e9, 50e9, slice_bytes=1 << 20))
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+    # the gathered buffer holds every shard at its rows, byte for byte
+    assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_ag_gemm_nan_poison():
+    # remote rows start as NaN; a tile read before its partition's flag would
+    # carry NaN into C
+    n = 8
+    M, N, K = 4096, 512, 512
+    inp = make_ag_inputs(M, N, K, n, seed=8)
+    case = AGCase(inp, 3, "double")
+    rows = M // n
+    for it in range(3):
+        for q in range(n):
+            if q != 3:
+                case.gathered[q * rows:(q + 1) * rows] = 0x7FC0   # bf16 quiet NaN
+        torch.cuda.synchronize()
+        _say("nan poison iteration", it)
+        C.compass_ag_gemm(case.problem, C.links(20e9, 20e9, slice_bytes=1 << 20))
+        C.compass_sync()
+        got = host_f64(case.C)
+        assert not np.isnan(got).any()
+        assert rel_err(got, case.reference()) < TOL
+
+
+# ------------------------------------------------------------ fused GEMM+ReduceScatter
+@pytest.mark.parametrize("ring", ["single", "double"])
+@pytest.mark.parametrize("n", [2, 4, 8])
+def test_gemm_rs_integer_exact(ring, n):
+    M, N, K = 128 * n, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=20 + n)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    rows = M // n
+    for r in sorted({0, n - 1, n // 2}):
+        _say("rs int", ring, n, r)
+        case = RSCase(inp, r, ring)
+        C.compass_gemm_rs(case.problem, FAST)
+        C.compass_sync()
+        got = host_bits(case.C)
+        assert np.array_equal(got, ref), f"rank {r}"
+        for q in range(n):
+            if q != r:
+                assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
+
+
+def test_gemm_rs_random_ragged_no_sends():
+    n = 4
+    M, N, K = 1024, 776, 1032
+    inp = make_rs_inputs(M, N, K, n, seed=31)
+    case = RSCase(inp, 2, "single", sends=False)
+    _say("rs ragged")
+    C.compass_gemm_rs(case.problem, FAST)
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+
+
+# ------------------------------------------------------------ InterDecom
+@pytest.mark.parametrize("ring", ["single", "double"])
+@pytest.mark.parametrize("d", [1, 2, 4, 8])
+def test_decomp_ag_integer_exact(ring, d):
+    n = 4
+    M, N, K = 1024, 264, 136
+    inp = make_int_ag_inputs(M, N, K, n, seed=40 + d)
+    ref = O.f64_to_bf16_rne(O.decomp_ag([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"]), d))
+    case = AGCase(inp, 1, ring)
+    _say("decomp ag", ring, d)
+    C.compass_decomp_gemm(case.problem, d, FAST)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), ref)
+
+
+@pytest.mark.parametrize("d", [1, 2, 4])
+def test_decomp_rs_integer_exact(d):
+    n = 4
+    M, N, K = 1024, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=50 + d)
+    ref = O.f64_to_bf16_rne(O.decomp_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                        [p.astype(np.float64) for p in inp["P_in"]], n, d))
+    case = RSCase(inp, 0, "single")
+    _say("decomp rs", d)
+    C.compass_decomp_gemm(case.problem, d, FAST)
+    C.compass_sync()
+    got = host_bits(case.C)
+    assert np.array_equal(got, ref)
+    rows = M // n
+    for q in range(1, n):
+        assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows])
+
+
+def test_decomp_rejects_bad_degree():
+    inp = make_int_ag_inputs(512, 64, 64, 4, seed=1)
+    case = AGCase(inp, 0, "single")
+    with pytest.raises(C.CompassError) as e:
+        C.compass_decomp_gemm(case.problem, 3, FAST)
+    assert e.value.code == C.ERR_INVALID
+
+
+# ------------------------------------------------------------ measurement companions
+def test_transfer_moves_every_shard():
+    n = 8
+    M, N, K = 2048, 256, 512
+    inp = make_ag_inputs(M, N, K, n, seed=60)
+    case = AGCase(inp, 5, "double")
+    _say("transfer ag")
+    C.compass_transfer(case.problem, FAST)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_sequential_ag_and_rs():
+    n = 4
+    inp = make_ag_inputs(1024, 264, 200, n, seed=61)
+    case = AGCase(inp, 2, "double")
+    _say("sequential ag")
+    C.compass_sequential(case.problem, FAST)
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+    rinp = make_rs_inputs(1024, 264, 200, n, seed=62)
+    rcase = RSCase(rinp, 1, "single")
+    # the sequential ReduceScatter's epilogue reads the staged partials as they
+    # are at launch: stage them with a transfer first
+    C.compass_transfer(rcase.problem, FAST)
+    C.compass_sync()
+    _say("sequential rs")
+    C.compass_sequential(rcase.problem, FAST)
+    C.compass_sync()
+    assert rel_err(host_f64(rcase.C), rcase.reference()) < TOL
+
+
+# ------------------------------------------------------------ failure handling
+def test_never_arriving_partition_times_out_then_recovers():
+    n = 4
+    inp = make_ag_inputs(1024, 256, 256, n, seed=70)
+    case = AGCase(inp, 0, "single")
+    C.compass_set_option(C.OPT_SPIN_LIMIT, 20000)
+    C.compass_set_option(C.OPT_DROP_FLAG, 2)
+    try:
+        _say("timeout case")
+        C.compass_ag_gemm(case.problem, FAST)
+        with pytest.raises(C.CompassError) as e:
+            C.compass_sync()
+        assert e.value.code == C.ERR_TIMEOUT
+    finally:
+        C.compass_set_option(C.OPT_DROP_FLAG, -1)
+        C.compass_set_option(C.OPT_SPIN_LIMIT, 4 << 20)
+    _say("recovery case")
+    C.compass_ag_gemm(case.problem, FAST)
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+
+
+def test_invalid_shapes_rejected_before_enqueue():
+    inp = make_int_ag_inputs(96, 64, 64, 4, seed=1)
+    case = AGCase(inp, 0, "single")
+    st = case.problem.st
+    st.K = 60   # not a multiple of 8
+    with pytest.raises(C.CompassError) as e:
+        C.compass_ag_gemm(case.problem, FAST)
+    assert e.value.code == C.ERR_INVALID
+    st.K = 64
+    st.rank = 7
+    with pytest.raises(C.CompassError):
+        C.compass_ag_gemm(case.problem, FAST)
