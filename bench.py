@@ -1,0 +1,284 @@
+#!/usr/bin/env python3
+"""Benchmark of the Compass hot path on one MI355X.
+
+One step = one tensor-parallel rank's share (TP = 8) of an MLP forward:
+  fc1  AllGather + GEMM   M=8192 (seq 2048 x batch 4), K=4096, N=2048,
+       double ring (A gathered from 8 row chunks of 1024 x 4096)
+  fc2  GEMM + ReduceScatter  M=8192, K=2048, N=4096, single ring, every
+       1024-row chunk summed with an fp32 incoming partial before its store
+For each operator, compass_pick_strategy (Algorithm 1, calibrated model)
+chooses TA-IntraFusion or ODP-InterDecom(d*), and the chosen operator runs
+through the C ABI with the other ranks emulated by paced SDMA copies from
+separate HBM buffers. Inputs are seeded synthetic tensors already resident in
+HBM. The value is whole-step throughput: 2*M*N*K of both GEMMs per second.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6      # 256 CUs x 4096 flop/clk x 2.4 GHz, dense
+LAMBDA_TARGET = 1.0            # link rates chosen so transfer time ~ GEMM time
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--strategy", choices=["auto", "fusion", "decomp", "sequential"], default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run only the timed steps (for rocprofv3); print the JSON line")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_10549_amd import calibrate as CAL
+    from paper_2609_10549_amd import compass as C
+    from synth import make_config_inputs
+
+    def say(*a):
+        print(*a, file=sys.stderr, flush=True)
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    rank = 0
+
+    # ---------------------------------------------------------------- inputs
+    say("bench: generating inputs")
+    ag_in = make_config_inputs(2)
+    rs_in = make_config_inputs(3)
+
+    def bits(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(dev)
+
+    n = ag_in["n"]
+    M1, N1, K1 = ag_in["M"], ag_in["N"], ag_in["K"]
+    rows1 = M1 // n
+    gathered = torch.empty((M1, K1), dtype=torch.int16, device=dev)
+    gathered[rank * rows1:(rank + 1) * rows1] = bits(ag_in["shards"][rank])
+    shards = [gathered[rank * rows1:(rank + 1) * rows1] if q == rank else bits(ag_in["shards"][q])
+              for q in range(n)]
+    W1 = bits(ag_in["W"])
+    C1 = torch.empty((M1, N1), dtype=torch.int16, device=dev)
+    p_ag = C.ag_problem(shards, gathered, W1, C1, rank, "double")
+
+    M2, N2, K2 = rs_in["M"], rs_in["N"], rs_in["K"]
+    rows2 = M2 // n
+    A2 = bits(rs_in["A"])
+    W2 = bits(rs_in["W"])
+    C2 = torch.empty((M2, N2), dtype=torch.int16, device=dev)
+    stage = torch.empty((M2, N2), dtype=torch.float32, device=dev)
+    partials = [torch.from_numpy(p).to(dev) for p in rs_in["P_in"]]
+    # the first ReduceScatter step's partial is resident: point it at its stage rows
+    first = C.compass_schedule("rs", "single", n, rank)[0]
+    stage[first * rows2:(first + 1) * rows2] = partials[first]
+    partials[first] = stage[first * rows2:(first + 1) * rows2]
+    sends = [None if q == rank else torch.empty((rows2, N2), dtype=torch.int16, device=dev) for q in range(n)]
+    p_rs = C.rs_problem(A2, W2, partials, stage, C2, sends, rank, "single")
+    torch.cuda.synchronize()
+
+    flops1 = 2.0 * M1 * N1 * K1
+    flops2 = 2.0 * M2 * N2 * K2
+
+    # ---------------------------------------------------------------- base times
+    say("bench: GEMM-alone and transfer-alone times")
+    t_gemm1 = CAL.time_call(lambda: C.compass_gemm(gathered, W1, C1), reps=10, warmup=3)
+    t_gemm2 = CAL.time_call(lambda: C.compass_gemm(A2, W2, C2, stage), reps=10, warmup=3)
+    per_link1 = CAL.ring_bytes_per_link("ag", M1, N1, K1, n, "double")
+    per_link2 = CAL.ring_bytes_per_link("rs", M2, N2, K2, n, "single")
+    unpaced = C.links(0.0, 0.0)
+    t_x1_max = CAL.time_call(lambda: C.compass_transfer(p_ag, unpaced), reps=5)
+    t_x2_max = CAL.time_call(lambda: C.compass_transfer(p_rs, unpaced), reps=5)
+    # link rates for lambda ~ 1, capped by what the copy engines sustain
+    rate1 = per_link1 / (t_gemm1 / LAMBDA_TARGET)
+    rate2 = per_link2 / (t_gemm2 / LAMBDA_TARGET)
+    cap1, cap2 = per_link1 / t_x1_max, per_link2 / t_x2_max
+    lk1 = C.links(rate1, rate1) if rate1 < 0.95 * cap1 else unpaced
+    lk2 = C.links(rate2, rate2) if rate2 < 0.95 * cap2 else unpaced
+    t_x1 = CAL.time_call(lambda: C.compass_transfer(p_ag, lk1), reps=5)
+    t_x2 = CAL.time_call(lambda: C.compass_transfer(p_rs, lk2), reps=5)
+
+    # ---------------------------------------------------------------- strategy (Algorithm 1)
+    cal = CAL.load()
+    if cal is None:
+        say("bench: no stored calibration, calibrating (quick)")
+        cal, _ = CAL.run(CAL.QUICK, verbose=False)
+    eff1 = per_link1 / t_x1
+    eff2 = per_link2 / t_x2
+
+    def choose(pattern, M, N, K, ring, rate):
+        w = C.compass_workload(pattern=C.PATTERNS[pattern], M=M, N=N, K=K, n=n)
+        t = C.compass_topology(ring=C.RINGS[ring], fwd_Bps=rate, bwd_Bps=rate, step_latency_s=0.0)
+        return C.compass_pick_strategy(w, t, cal)
+
+    ch1 = choose("ag", M1, N1, K1, "double", eff1)
+    ch2 = choose("rs", M2, N2, K2, "single", eff2)
+
+    def op_for(strategy, choice, fused, prob, lk):
+        if strategy == "fusion" or (strategy == "auto" and choice.strategy == C.INTRA_FUSION):
+            return ("intra_fusion", 1, lambda: fused(prob, lk))
+        if strategy == "sequential":
+            return ("sequential", 1, lambda: C.compass_sequential(prob, lk))
+        d = max(choice.d_star, 2) if strategy == "decomp" else choice.d_star
+        return ("inter_decom", d, lambda: C.compass_decomp_gemm(prob, d, lk))
+
+    s1, d1, f1 = op_for(args.strategy, ch1, C.compass_ag_gemm, p_ag, lk1)
+    s2, d2, f2 = op_for(args.strategy, ch2, C.compass_gemm_rs, p_rs, lk2)
+
+    def step():
+        f1()
+        f2()
+
+    # ---------------------------------------------------------------- timed steps
+    say(f"bench: warmup {args.warmup}, fc1 {s1} d={d1}, fc2 {s2} d={d2}")
+    for _ in range(args.warmup):
+        step()
+    C.compass_sync()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    say(f"bench: timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record()
+        f1()
+        ev[k][1].record()
+        f2()
+        ev[k][2].record()
+    torch.cuda.synchronize()
+    C.compass_sync()
+    wall = time.perf_counter() - t0
+    op1 = [ev[k][0].elapsed_time(ev[k][1]) * 1e-3 for k in range(args.steps)]
+    op2 = [ev[k][1].elapsed_time(ev[k][2]) * 1e-3 for k in range(args.steps)]
+    ms_per_step = wall / args.steps * 1e3
+    t_op1, t_op2 = float(np.mean(op1)), float(np.mean(op2))
+    value = (flops1 + flops2) / (wall / args.steps) / 1e12
+
+    # dominant kernel: the GEMM kernel of the longer operator
+    if t_op1 >= t_op2:
+        dom = dict(name=f"gemm_kernel<AllGather> ({s1})", flops=flops1, t=t_op1)
+    else:
+        dom = dict(name=f"gemm_kernel<ReduceScatter> ({s2}, incl. send join)", flops=flops2, t=t_op2)
+    achieved = dom["flops"] / dom["t"] / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom["name"]}
+
+    result = {
+        "metric": "AG-GEMM/GEMM-RS TFLOP/s + overlap efficiency vs unfused GEMM+copy, 1 GPU",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "tp8_mlp_fwd_rank_share: fc1 AG-GEMM 8192x2048x4096 double ring + "
+                               "fc2 GEMM-RS 8192x4096x2048 single ring",
+                   "global_batch": 4, "seq_len": 2048, "parallelism": "tp8 (one rank emulated)"},
+        "roofline": roofline,
+    }
+    if args.profile_only:
+        print(json.dumps(result))
+        return
+
+    # ---------------------------------------------------------------- overlap efficiency (untimed region)
+    say("bench: unfused and fused references")
+    t_seq1 = CAL.time_call(lambda: C.compass_sequential(p_ag, lk1), reps=5)
+    t_seq2 = CAL.time_call(lambda: C.compass_sequential(p_rs, lk2), reps=5)
+    t_fus1 = CAL.time_call(lambda: C.compass_ag_gemm(p_ag, lk1), reps=5)
+    t_fus2 = CAL.time_call(lambda: C.compass_gemm_rs(p_rs, lk2), reps=5)
+
+    def overlap(t_unf, t_fus, tg, tx):
+        ideal = t_unf - max(tg, tx)
+        E = (t_unf - t_fus) / ideal if ideal > 0 else None
+        h = (tg + tx - t_fus) / tx
+        return E, h
+
+    E1, h1 = overlap(t_seq1, t_fus1, t_gemm1, t_x1)
+    E2, h2 = overlap(t_seq2, t_fus2, t_gemm2, t_x2)
+    rnd = lambda x, k=4: None if x is None else round(x, k)  # noqa: E731
+    result["ops"] = {
+        "fc1_ag": {"strategy": s1, "d": d1, "t_op_us": rnd(t_op1 * 1e6, 2), "tflops": rnd(flops1 / t_op1 / 1e12, 1),
+                   "t_gemm_us": rnd(t_gemm1 * 1e6, 2), "gemm_tflops": rnd(flops1 / t_gemm1 / 1e12, 1),
+                   "t_xfer_us": rnd(t_x1 * 1e6, 2), "t_fused_us": rnd(t_fus1 * 1e6, 2),
+                   "t_unfused_us": rnd(t_seq1 * 1e6, 2), "lambda": rnd(t_gemm1 / t_x1, 3),
+                   "overlap_efficiency": rnd(E1), "transfer_hidden": rnd(h1),
+                   "link_Bps_per_ring": rnd(per_link1 / t_x1, 0), "link_paced": lk1.fwd_Bps > 0,
+                   "link_ceiling_Bps_per_ring": rnd(cap1, 0),
+                   "model": {"d_star": ch1.d_star, "t_fusion_us": rnd(ch1.t_fusion * 1e6, 2),
+                             "t_decomp_us": rnd(ch1.t_decomp * 1e6, 2), "lambda": rnd(ch1.lambda_, 3)}},
+        "fc2_rs": {"strategy": s2, "d": d2, "t_op_us": rnd(t_op2 * 1e6, 2), "tflops": rnd(flops2 / t_op2 / 1e12, 1),
+                   "t_gemm_us": rnd(t_gemm2 * 1e6, 2), "gemm_tflops": rnd(flops2 / t_gemm2 / 1e12, 1),
+                   "t_xfer_us": rnd(t_x2 * 1e6, 2), "t_fused_us": rnd(t_fus2 * 1e6, 2),
+                   "t_unfused_us": rnd(t_seq2 * 1e6, 2), "lambda": rnd(t_gemm2 / t_x2, 3),
+                   "overlap_efficiency": rnd(E2), "transfer_hidden": rnd(h2),
+                   "link_Bps_per_ring": rnd(per_link2 / t_x2, 0), "link_paced": lk2.fwd_Bps > 0,
+                   "link_ceiling_Bps_per_ring": rnd(cap2, 0),
+                   "model": {"d_star": ch2.d_star, "t_fusion_us": rnd(ch2.t_fusion * 1e6, 2),
+                             "t_decomp_us": rnd(ch2.t_decomp * 1e6, 2), "lambda": rnd(ch2.lambda_, 3)}},
+    }
+
+    # ---------------------------------------------------------------- CPU baseline (the oracle)
+    if not args.no_cpu_baseline:
+        say("bench: CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(ag_in, rs_in)
+    print(json.dumps(result))
+
+
+def cpu_baseline(ag_in, rs_in) -> dict:
+    """The fp64 oracle on a bounded sample of the same step: the first
+    `rows` rows of every fc1 shard gathered and multiplied, and the same rows
+    of every fc2 chunk multiplied and reduced; repeated until about 10 s of
+    CPU work. Scaled to TFLOP/s of the sampled flops."""
+    import numpy as np
+
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    n = ag_in["n"]
+    rows = 256
+    sh = [s[:rows] for s in ag_in["shards"]]
+    W1 = ag_in["W"]
+    rows2 = rs_in["M"] // n
+    idx = np.concatenate([np.arange(c * rows2, c * rows2 + rows) for c in range(n)])
+    A2 = rs_in["A"][idx]
+    P2 = [p[:rows] for p in rs_in["P_in"]]
+    W2 = rs_in["W"]
+    flops = 2.0 * (n * rows) * ag_in["N"] * ag_in["K"] + 2.0 * (n * rows) * rs_in["N"] * rs_in["K"]
+    times = []
+    t_all = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        O.ag_gemm([O.bf16_to_f64(s) for s in sh], O.bf16_to_f64(W1))
+        O.gemm_rs(O.bf16_to_f64(A2), O.bf16_to_f64(W2), [p.astype(np.float64) for p in P2], n)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_all > 10.0 or len(times) >= 50:
+            break
+    t = float(np.median(times))
+    return {"value": round(flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{rows} rows of each of the {n} fc1 shards and fc2 chunks (1/{rows2 // rows} of a step), "
+                      f"fp64 numpy, median of {len(times)} runs"}
+
+
+if __name__ == "__main__":
+    main()

@@ -193,6 +193,10 @@ int compass_sync(void);
 #define COMPASS_OPT_GRID         3  /* persistent grid size; 0 = one workgroup per CU */
 #define COMPASS_OPT_DROP_FLAG    4  /* test only: index of an AllGather partition whose
                                        copy and flag are never issued; -1 = none */
+#define COMPASS_OPT_TILE         5  /* GEMM tile: 0 = chosen per operator, 1 = 256 x 256
+                                       (one workgroup per CU), 2 = 128 x 128 (two) */
+#define COMPASS_OPT_ENGINE_MASK  6  /* bit i set: SDMA engine i may carry emulated link
+                                       traffic; 0 = every engine that accepts a copy */
 int compass_set_option(int key, long long value);
 
 /* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */

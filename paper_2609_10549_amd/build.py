@@ -49,7 +49,7 @@ def build(verbose: bool = False) -> str:
         objs.append(obj)
     tmp = LIB + ".tmp"
     cmd = [HIPCC] + DEVICE_FLAGS + ["-shared", "-fPIC", "-o", tmp] + objs + \
-        ["-L/opt/rocm/lib", "-lhsa-runtime64", "-lamdhip64", "-lpthread", "-Wl,-rpath,/opt/rocm/lib"]
+        ["-L/opt/rocm/lib", "-lhsa-runtime64", "-lamdhip64", "-lpthread", "-rdynamic", "-Wl,-rpath,/opt/rocm/lib"]
     _run(cmd)
     os.replace(tmp, LIB)
     shutil.rmtree(objdir, ignore_errors=True)

@@ -1,0 +1,152 @@
+"""Offline calibration of the Compass model on this GPU (Section IV-C:
+one-time linear regression of the overhead parameters).
+
+    python -m paper_2609_10549_amd.calibrate [--out calibration.json] [--quick]
+
+Measures, through the C ABI only:
+  * plain GEMM times over a set of shapes          -> T_comp = a + b * 2MNK
+  * InterDecom times at d = 2..16 with the GEMM-alone and transfer-alone
+    times of the same workload                     -> eta(d) = alpha + beta d
+  * fused (IntraFusion) times with the same base   -> overhead alpha_f + beta_f m
+and fits them with compass_calibrate. The shapes come from the Table IV grid
+(those that fit one GPU's share at TP = 8), so the fit never uses the exact
+evaluation workloads of the benchmark.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+
+import numpy as np
+import torch
+
+from . import compass as C
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+DEFAULT_OUT = os.path.join(HERE, "calibration.json")
+
+# (pattern, M, N, K, n): Table IV values of M, N, K at TP = 8
+SHAPES = [
+    ("ag", 2048, 2048, 4096, 8), ("ag", 4096, 4096, 4096, 8), ("ag", 8192, 4096, 8192, 8),
+    ("ag", 12288, 2048, 8192, 8), ("ag", 16384, 2048, 4096, 8),
+    ("rs", 2048, 4096, 2048, 8), ("rs", 4096, 8192, 2048, 8), ("rs", 12288, 4096, 4096, 8),
+    ("rs", 16384, 8192, 2048, 8),
+]
+QUICK = [SHAPES[0], SHAPES[2], SHAPES[5], SHAPES[7]]
+
+
+def _rand_bits(shape, gen):
+    # small random bf16 patterns (values in about [-2, 2]); calibration only needs timing
+    x = torch.randn(shape, device="cuda", generator=gen, dtype=torch.float32)
+    return x.to(torch.bfloat16).view(torch.int16)
+
+
+class Buffers:
+    def __init__(self, pattern, M, N, K, n, ring, rank=0):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(M * 7 + N * 3 + K)
+        rows = M // n
+        self.pattern = pattern
+        self.W = _rand_bits((N, K), g)
+        self.C = torch.empty((M, N), dtype=torch.int16, device="cuda")
+        if pattern == "ag":
+            self.gathered = _rand_bits((M, K), g)
+            self.shards = [self.gathered[q * rows:(q + 1) * rows] if q == rank else _rand_bits((rows, K), g)
+                           for q in range(n)]
+            self.problem = C.ag_problem(self.shards, self.gathered, self.W, self.C, rank, ring)
+            self.A = self.gathered
+            self.P = None
+        else:
+            self.A = _rand_bits((M, K), g)
+            self.stage = torch.randn((M, N), device="cuda", generator=g)
+            self.partials = [torch.randn((rows, N), device="cuda", generator=g) for _ in range(n)]
+            self.send = [None if q == rank else torch.empty((rows, N), dtype=torch.int16, device="cuda")
+                         for q in range(n)]
+            self.problem = C.rs_problem(self.A, self.W, self.partials, self.stage, self.C, self.send, rank, ring)
+            self.P = self.stage
+
+
+def time_call(fn, reps=5, warmup=2) -> float:
+    """Median seconds of fn() measured with HIP events on the current stream."""
+    for _ in range(warmup):
+        fn()
+    C.compass_sync()
+    out = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        out.append(a.elapsed_time(b) * 1e-3)
+    C.compass_sync()
+    return float(np.median(out))
+
+
+def ring_bytes_per_link(pattern, M, N, K, n, ring):
+    """Bytes one ring link carries in the whole collective (n-1 steps)."""
+    div = n if ring == "single" else 2 * n
+    per = M * K * 2 / div if pattern == "ag" else M * N * 4 / div
+    return (n - 1) * per
+
+
+def run(shapes, ds=(2, 4, 8, 16), lam_targets=(0.5, 1.0, 2.0), ring="double", verbose=True):
+    samples = []
+    rows_out = []
+    for (pat, M, N, K, n) in shapes:
+        buf = Buffers(pat, M, N, K, n, ring)
+        w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+        tg = time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P))
+        samples.append(C.compass_sample(kind=0, w=w, d=1, t_meas=tg, t_comp=tg, t_comm=0.0))
+        per_link = ring_bytes_per_link(pat, M, N, K, n, ring)
+        for lam in lam_targets:
+            rate = per_link / (tg / lam)
+            lk = C.links(rate, rate)
+            tx = time_call(lambda: C.compass_transfer(buf.problem, lk))
+            tf = time_call(lambda: (C.compass_ag_gemm if pat == "ag" else C.compass_gemm_rs)(buf.problem, lk))
+            samples.append(C.compass_sample(kind=2, w=w, d=1, t_meas=tf, t_comp=tg, t_comm=tx))
+            rec = dict(pattern=pat, M=M, N=N, K=K, n=n, lam_target=lam, rate=rate, t_gemm=tg, t_xfer=tx, t_fused=tf)
+            for d in ds:
+                if (M // n) % (2 * d if ring == "double" else d):
+                    continue
+                td = time_call(lambda: C.compass_decomp_gemm(buf.problem, d, lk))
+                samples.append(C.compass_sample(kind=1, w=w, d=d, t_meas=td, t_comp=tg, t_comm=tx))
+                rec[f"t_decomp_{d}"] = td
+            rows_out.append(rec)
+            if verbose:
+                print(json.dumps(rec), flush=True)
+        del buf
+        torch.cuda.empty_cache()
+    cal = C.compass_calibrate(samples, C.compass_calib(d_max=16))
+    return cal, rows_out
+
+
+def calib_to_dict(cal) -> dict:
+    return {k: getattr(cal, k) for k, _ in cal._fields_}
+
+
+def load(path: str = DEFAULT_OUT):
+    """The stored calibration as a compass_calib, or None."""
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)["calib"]
+    return C.compass_calib(**d)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=DEFAULT_OUT)
+    ap.add_argument("--quick", action="store_true")
+    args = ap.parse_args()
+    cal, rows = run(QUICK if args.quick else SHAPES)
+    d = calib_to_dict(cal)
+    with open(args.out, "w") as f:
+        json.dump({"calib": d, "measurements": rows, "device": torch.cuda.get_device_name(0)}, f, indent=1)
+    print(json.dumps(d))
+
+
+if __name__ == "__main__":
+    main()

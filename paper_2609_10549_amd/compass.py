@@ -31,6 +31,8 @@ OPT_SPIN_LIMIT = 1
 OPT_HOST_TIMEOUT = 2
 OPT_GRID = 3
 OPT_DROP_FLAG = 4
+OPT_TILE = 5
+OPT_ENGINE_MASK = 6
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE}

@@ -4,15 +4,24 @@
 
 namespace compass {
 
-constexpr int kTileM = 256;          // output tile rows (M)
-constexpr int kTileN = 256;          // output tile columns (N)
 constexpr int kTileK = 64;           // K depth of one LDS stage
-constexpr int kThreads = 256;        // 4 waves of 64
-constexpr int kMaxRowTiles = 256;    // M up to 65536 rows per launch
+constexpr int kThreads = 256;        // 4 waves of 64, 2 x 2 over the tile
+constexpr int kMaxRowTiles = 512;    // row tiles per launch
 constexpr int kMaxParts = 64;        // partitions per launch (2 n, n <= 32)
 constexpr int kMaxFlags = 2048;      // arrival / done flag slots
 constexpr int kFinalFlag0 = kMaxFlags - 8;  // end-of-job flags
 constexpr int kMaxJoin = 80;
+constexpr int kMaxQueues = 8;        // ticket queues (one per XCD)
+constexpr int kCtrlExit = kMaxQueues;       // ctrl word: exit counter
+
+// Tile configurations of the GEMM kernel.
+enum TileCfg : int {
+    kTile256 = 0,   // 256 x 256 output tile, 128 KiB LDS, one workgroup per CU
+    kTile128 = 1,   // 128 x 128 output tile, 64 KiB LDS, two workgroups per CU
+};
+inline int tile_rows(int cfg) { return cfg == kTile256 ? 256 : 128; }
+inline int tile_cols(int cfg) { return cfg == kTile256 ? 256 : 128; }
+inline int tile_wg_per_cu(int cfg) { return cfg == kTile256 ? 1 : 2; }
 
 // Where a tile waits for its partitions' arrival flags.
 enum GateMode : int {
@@ -34,8 +43,18 @@ struct GemmParams {
     // logical row i -> physical row (i / piece) * pstride + poff + i % piece;
     // piece == 0 means the identity map
     int piece, pstride, poff;
-    // gating: flag index of partition p is flag_base + p
-    uint32_t *flags;         // arrival flags (fine-grained device memory)
+    // tile distribution: queue v = blockIdx % nq takes super-blocks
+    // v, v + nq, ... of q_size consecutive positions of the ready order;
+    // positions walk group_m row tiles before the next column tile
+    int nq, q_size, group_m;
+    int grid;
+    // gating: flag index of partition p is flag_base + p. Arrival flags live
+    // in pinned host memory (written by the copy-side threads); the first
+    // workgroup that needs a partition in an epoch (`leader`) polls it and
+    // copies it into `mirror` (device memory), which the others poll.
+    uint32_t *flags;
+    uint32_t *mirror;
+    uint32_t *leader;
     int gate;                // GateMode
     int flag_base;
     int nparts;              // partitions used by this launch
@@ -47,12 +66,12 @@ struct GemmParams {
     uint32_t *done_cnt;      // device counters, indexed like flags
     uint32_t *done_host;     // host-visible done flags, indexed like flags
     // control
-    uint32_t *ctrl;          // [0] tile ticket, [1] exit counter
+    uint32_t *ctrl;          // [0, nq) tickets, [kCtrlExit] exit counter
     uint32_t *start_word;    // host-visible; written with epoch at start (or null)
     uint32_t *err_word;      // host-visible error word
-    int grid;
-    uint16_t rt_order[kMaxRowTiles];   // processing order of the row tiles
-    uint64_t rt_touch[kMaxRowTiles];   // partitions each row tile depends on
+    uint16_t rt_order[kMaxRowTiles];   // ready order of the row tiles
+    uint8_t rt_lo[kMaxRowTiles];       // partitions [lo, hi] a row tile depends on
+    uint8_t rt_hi[kMaxRowTiles];
     uint32_t done_expect[kMaxParts];   // tiles per partition to count (0: none)
 };
 

@@ -5,10 +5,11 @@
 // (HSA async copies forced onto SDMA, so no compute unit is taken from the
 // GEMM). A job is an ordered list of partition transfers; the pacer issues
 // them in slices no earlier than their paced times (rate = the emulated link
-// bandwidth), and after the last slice of a partition it appends a 4-byte
-// copy of the call's epoch into that partition's arrival flag, dependent on
-// the partition's slices. The GEMM kernel polls those flags (fine-grained
-// device memory) with system-scope acquire loads.
+// bandwidth), polls the slices' completion signals, and publishes a
+// partition's arrival flag (a release store of the call's epoch into pinned
+// host memory) once all of its slices have landed. Copies never depend on one
+// another through signals: every completion signal is re-armed only after the
+// copy it tracked has completed.
 //
 // Operators (Section III-B TA-IntraFusion, Section II-B / IV InterDecom) are
 // built from one persistent GEMM launch (or d launches) plus these jobs. Row
@@ -20,7 +21,10 @@
 #include <hip/hip_runtime.h>
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
+#include <execinfo.h>
 #include <immintrin.h>
+#include <signal.h>
+#include <unistd.h>
 
 #include <algorithm>
 #include <atomic>
@@ -43,7 +47,7 @@
 
 namespace compass {
 
-hipError_t launch_gemm(const GemmParams &p, bool rs, hipStream_t stream);
+hipError_t launch_gemm(const GemmParams &p, int cfg, bool rs, hipStream_t stream);
 hipError_t launch_join(const JoinParams &j, hipStream_t stream);
 
 // ---------------------------------------------------------------- errors
@@ -67,15 +71,17 @@ static double now_s() {
 
 // ---------------------------------------------------------------- state
 constexpr int kRoles = 4;            // in-fwd, in-bwd, out-fwd, out-bwd
-constexpr int kSignals = 512;        // completion signals per pacer
-constexpr int kEpochSlots = 256;
+constexpr int kSignals = 256;        // completion signals per pacer
 constexpr size_t kDefaultSlice = 4u << 20;
-// host_words layout (pinned, coherent host memory)
-constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwEpoch = kHwDone + kMaxFlags;
-constexpr int kHwWords = kHwEpoch + kEpochSlots;
-// ctrl layout (device memory)
+// host_words layout (pinned, coherent host memory): start word, error word,
+// done flags (kernel -> copy side), arrival flags (copy side -> kernel)
+constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
+constexpr int kHwWords = kHwFlags + kMaxFlags;
+// ctrl layout (device memory): tickets, done counters, flag mirrors, leaders
 constexpr int kCtrlDone = 64;
-constexpr int kCtrlWords = kCtrlDone + kMaxFlags;
+constexpr int kCtrlMirror = kCtrlDone + kMaxFlags;
+constexpr int kCtrlLeader = kCtrlMirror + kMaxFlags;
+constexpr int kCtrlWords = kCtrlLeader + kMaxFlags;
 
 struct Item {
     void *dst;
@@ -100,6 +106,7 @@ struct Ctx;
 
 struct Pacer {
     Ctx *ctx = nullptr;
+    int role = 0;
     std::thread th;
     std::mutex mu;
     std::condition_variable cv;
@@ -119,7 +126,6 @@ struct Ctx {
     int num_cu = 0;
     hsa_agent_t gpu{}, cpu{};
     std::vector<uint32_t> engines;   // SDMA engines usable device->device
-    uint32_t *flags = nullptr;       // fine-grained device memory
     uint32_t *ctrl = nullptr;        // device memory
     uint32_t *hw = nullptr;          // pinned host words
     uint32_t epoch = 0;
@@ -129,6 +135,13 @@ struct Ctx {
     double host_timeout = 5.0;       // seconds
     int grid_override = 0;
     int drop_flag = -1;
+    int tile_override = 0;           // 0 auto, 1 256 x 256, 2 128 x 128
+    uint32_t engine_mask = 0;        // hardware engines allowed (0: all usable)
+    // copy-side trace (COMPASS_TRACE=<file>): one line per event
+    bool tracing = false;
+    std::string trace_path;
+    std::mutex trace_mu;
+    std::vector<std::string> trace;
     struct Range { uintptr_t lo, hi; hsa_agent_t owner; };
     std::vector<Range> ranges;       // pointer -> owning agent cache
     ~Ctx();
@@ -145,6 +158,34 @@ Ctx::~Ctx() {
     }
     for (auto &p : pacer)
         if (p.th.joinable()) p.th.join();
+    if (tracing && !trace.empty()) {
+        if (FILE *f = std::fopen(trace_path.c_str(), "w")) {
+            std::fputs("t_s,role,epoch,event,item,bytes\n", f);
+            for (auto &l : trace) std::fputs(l.c_str(), f);
+            std::fclose(f);
+        }
+    }
+}
+
+static void trace_event(int role, uint32_t epoch, const char *ev, int item, size_t bytes) {
+    Ctx &c = g_ctx;
+    if (!c.tracing) return;
+    char buf[160];
+    std::snprintf(buf, sizeof buf, "%.9f,%d,%u,%s,%d,%zu\n", now_s(), role, epoch, ev, item, bytes);
+    std::lock_guard<std::mutex> lk(c.trace_mu);
+    if (c.trace.size() < 2000000) c.trace.push_back(buf);
+}
+
+// COMPASS_DEBUG_SEGV=1: print the native backtrace of a thread that faults
+// on the host, then fall back to the default action.
+static void segv_handler(int sig) {
+    void *frames[64];
+    const int n = backtrace(frames, 64);
+    static const char msg[] = "compass: host fault, native backtrace:\n";
+    (void)!write(2, msg, sizeof msg - 1);
+    backtrace_symbols_fd(frames, n, 2);
+    signal(sig, SIG_DFL);
+    raise(sig);
 }
 
 static hsa_status_t agent_cb(hsa_agent_t a, void *data) {
@@ -173,6 +214,10 @@ static int ensure_init() {
         return set_error(COMPASS_ERR_UNSUPPORTED, "device %d is %s, this library is built for gfx950", dev, prop.gcnArchName);
     c.device = dev;
     c.num_cu = prop.multiProcessorCount;
+    if (std::getenv("COMPASS_DEBUG_SEGV")) {
+        signal(SIGSEGV, segv_handler);
+        signal(SIGBUS, segv_handler);
+    }
     if (hsa_init() != HSA_STATUS_SUCCESS) return set_error(COMPASS_ERR_HIP, "hsa_init failed");
     std::vector<hsa_agent_t> agents;
     hsa_iterate_agents(agent_cb, &agents);
@@ -194,15 +239,17 @@ static int ensure_init() {
     }
     if (!found && (int)gpus.size() > dev) { c.gpu = gpus[dev]; found = true; }
     if (!found || !have_cpu) return set_error(COMPASS_ERR_HIP, "could not find the HSA agents");
-    if ((e = hipExtMallocWithFlags((void **)&c.flags, kMaxFlags * sizeof(uint32_t), hipDeviceMallocFinegrained)) != hipSuccess)
-        return hip_fail(e, "flag allocation");
     if ((e = hipMalloc((void **)&c.ctrl, kCtrlWords * sizeof(uint32_t))) != hipSuccess) return hip_fail(e, "control allocation");
     if ((e = hipHostMalloc((void **)&c.hw, kHwWords * sizeof(uint32_t), hipHostMallocCoherent)) != hipSuccess)
         return hip_fail(e, "host word allocation");
     std::memset(c.hw, 0, kHwWords * sizeof(uint32_t));
-    if ((e = hipMemset(c.flags, 0, kMaxFlags * sizeof(uint32_t))) != hipSuccess) return hip_fail(e, "flag clear");
     if ((e = hipMemset(c.ctrl, 0, kCtrlWords * sizeof(uint32_t))) != hipSuccess) return hip_fail(e, "control clear");
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "init sync");
+    for (int r = 0; r < kRoles; ++r) c.pacer[r].role = r;
+    if (const char *tp = std::getenv("COMPASS_TRACE")) {
+        c.tracing = true;
+        c.trace_path = tp;
+    }
     for (auto &p : c.pacer) {
         p.ctx = &c;
         for (auto &s : p.sig)
@@ -221,7 +268,7 @@ static int ensure_init() {
         for (int i = 0; i < 16; ++i) {
             const uint32_t id = 1u << i;
             hsa_signal_store_relaxed(s, 1);
-            if (hsa_amd_memory_async_copy_on_engine(c.flags + kMaxFlags - 1, c.gpu, c.flags + kMaxFlags - 2, c.gpu,
+            if (hsa_amd_memory_async_copy_on_engine(c.ctrl + kCtrlWords - 1, c.gpu, c.ctrl + kCtrlWords - 2, c.gpu,
                                                     sizeof(uint32_t), 0, nullptr, s, (hsa_amd_sdma_engine_id_t)id,
                                                     true) != HSA_STATUS_SUCCESS) {
                 hsa_signal_store_relaxed(s, 0);
@@ -235,8 +282,9 @@ static int ensure_init() {
             if (hsa_signal_load_scacquire(s) < 0) continue;
             (avail & id ? ok_free : ok_busy).push_back(id);
         }
+        // engines other clients hold are used only when fewer than four are free
         c.engines = ok_free;
-        c.engines.insert(c.engines.end(), ok_busy.begin(), ok_busy.end());
+        if (c.engines.size() < 4) c.engines.insert(c.engines.end(), ok_busy.begin(), ok_busy.end());
         if (c.engines.empty()) return set_error(COMPASS_ERR_UNSUPPORTED, "no SDMA engine accepted a copy");
         if (std::getenv("COMPASS_VERBOSE"))
             std::fprintf(stderr, "compass: %zu SDMA engines usable (%zu reported free)\n", c.engines.size(), ok_free.size());
@@ -319,90 +367,106 @@ static bool spin_until_epoch(volatile uint32_t *w, uint32_t epoch, double timeou
     return true;
 }
 
+// One job: issue every item's slices at their paced times (after the item's
+// gate opened), and publish an item's arrival flag, a release store of the
+// epoch into host memory, as soon as all of its slices have landed. Copies
+// carry no dependencies on one another; completion is observed here.
 void Pacer::execute(Job &job) {
     Ctx &c = *ctx;
     if (job.items.empty() && job.final_flag < 0) return;
+    trace_event(role, job.epoch, "job_begin", -1, 0);
     if (job.wait_start && !spin_until_epoch(&c.hw[kHwStart], job.epoch, c.host_timeout)) {
         c.async_err.store(COMPASS_ERR_TIMEOUT);
         return;
     }
+    trace_event(role, job.epoch, "start_seen", -1, 0);
+    struct Pend {
+        int flag;
+        size_t first, count;   // its signals in `issued`
+    };
     const size_t E = job.engines.size();
-    std::vector<hsa_signal_t> last(E);
-    std::vector<bool> used(E, false);
-    const uint32_t *epoch_src = &c.hw[kHwEpoch + job.epoch % kEpochSlots];
+    std::vector<hsa_signal_t> issued;
+    std::vector<Pend> pend;
     double t_next = now_s();
-    size_t rr = 0;
-    for (const Item &it : job.items) {
-        if (it.gate >= 0) {
-            if (!spin_until_epoch(&c.hw[kHwDone + it.gate], job.epoch, c.host_timeout)) {
+    double last_progress = t_next;
+    size_t rr = 0, idx = 0, off = 0, item_first = 0;
+    bool gate_ok = false;
+    for (;;) {
+        bool progress = false;
+        for (size_t i = 0; i < pend.size();) {
+            bool landed = true;
+            for (size_t k = pend[i].first; k < pend[i].first + pend[i].count && landed; ++k)
+                landed = hsa_signal_load_scacquire(issued[k]) <= 0;
+            if (landed) {
+                __atomic_store_n(&c.hw[kHwFlags + pend[i].flag], job.epoch, __ATOMIC_RELEASE);
+                trace_event(role, job.epoch, "flag", pend[i].flag, 0);
+                pend.erase(pend.begin() + (long)i);
+                progress = true;
+            } else {
+                ++i;
+            }
+        }
+        if (idx < job.items.size()) {
+            const Item &it = job.items[idx];
+            if (it.gate >= 0 && !gate_ok &&
+                (int32_t)(__atomic_load_n(&c.hw[kHwDone + it.gate], __ATOMIC_ACQUIRE) - job.epoch) >= 0) {
+                gate_ok = true;
+                t_next = std::max(t_next, now_s());
+                trace_event(role, job.epoch, "gate_open", it.gate, 0);
+            }
+            if ((it.gate < 0 || gate_ok) && (job.rate <= 0 || now_s() >= t_next)) {
+                if (off == 0) item_first = issued.size();
+                if (off < it.bytes) {
+                    const size_t len = std::min(job.slice, it.bytes - off);
+                    if (job.rate > 0) t_next += (double)len / job.rate;
+                    const size_t e = rr++ % E;
+                    hsa_signal_t sg = take_signal();
+                    const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
+                        (char *)it.dst + off, it.dst_agent, (const char *)it.src + off, it.src_agent, len, 0,
+                        nullptr, sg, (hsa_amd_sdma_engine_id_t)job.engines[e], true);
+                    if (st != HSA_STATUS_SUCCESS) {
+                        hsa_signal_store_relaxed(sg, 0);
+                        c.async_err.store(COMPASS_ERR_HIP);
+                        return;
+                    }
+                    trace_event(role, job.epoch, "slice", __builtin_ctz(job.engines[e]), len);
+                    issued.push_back(sg);
+                    off += len;
+                }
+                if (off >= it.bytes) {
+                    if (it.flag >= 0) pend.push_back({it.flag, item_first, issued.size() - item_first});
+                    ++idx;
+                    off = 0;
+                    gate_ok = false;
+                }
+                progress = true;
+            }
+        } else if (pend.empty()) {
+            break;
+        }
+        if (progress) {
+            last_progress = now_s();
+        } else {
+            if (now_s() - last_progress > c.host_timeout) {
                 c.async_err.store(COMPASS_ERR_TIMEOUT);
                 return;
             }
-            t_next = std::max(t_next, now_s());
-        }
-        std::vector<hsa_signal_t> deps;
-        std::vector<bool> item_used(E, false);
-        std::vector<hsa_signal_t> item_last(E);
-        size_t off = 0;
-        size_t e_last = 0;
-        while (off < it.bytes) {
-            const size_t len = std::min(job.slice, it.bytes - off);
-            if (job.rate > 0) {
-                while (now_s() < t_next) _mm_pause();
-                t_next += (double)len / job.rate;
-            }
-            const size_t e = rr++ % E;
-            hsa_signal_t s = take_signal();
-            const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
-                (char *)it.dst + off, it.dst_agent, (const char *)it.src + off, it.src_agent, len, 0, nullptr, s,
-                (hsa_amd_sdma_engine_id_t)job.engines[e], true);
-            if (st != HSA_STATUS_SUCCESS) {
-                hsa_signal_store_relaxed(s, 0);
-                c.async_err.store(COMPASS_ERR_HIP);
-                return;
-            }
-            last[e] = s; used[e] = true;
-            item_last[e] = s; item_used[e] = true;
-            e_last = e;
-            off += len;
-        }
-        if (it.flag >= 0) {
-            for (size_t e = 0; e < E; ++e)
-                if (item_used[e]) deps.push_back(item_last[e]);
-            hsa_signal_t s = take_signal();
-            const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
-                c.flags + it.flag, c.gpu, epoch_src, c.cpu, sizeof(uint32_t), (uint32_t)deps.size(),
-                deps.empty() ? nullptr : deps.data(), s, (hsa_amd_sdma_engine_id_t)job.engines[e_last], true);
-            if (st != HSA_STATUS_SUCCESS) {
-                hsa_signal_store_relaxed(s, 0);
-                c.async_err.store(COMPASS_ERR_HIP);
-                return;
-            }
-            last[e_last] = s;
-        }
-    }
-    std::vector<hsa_signal_t> deps;
-    for (size_t e = 0; e < E; ++e)
-        if (used[e]) deps.push_back(last[e]);
-    if (job.final_flag >= 0) {
-        hsa_signal_t s = take_signal();
-        const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
-            c.flags + job.final_flag, c.gpu, epoch_src, c.cpu, sizeof(uint32_t), (uint32_t)deps.size(),
-            deps.empty() ? nullptr : deps.data(), s, (hsa_amd_sdma_engine_id_t)job.engines[0], true);
-        if (st != HSA_STATUS_SUCCESS) {
-            hsa_signal_store_relaxed(s, 0);
-            c.async_err.store(COMPASS_ERR_HIP);
-            return;
-        }
-        deps.push_back(s);
-    }
-    // the job is over once its copies have landed
-    const double t0 = now_s();
-    for (auto s : deps)
-        while (hsa_signal_load_scacquire(s) > 0) {
-            if (now_s() - t0 > c.host_timeout) { c.async_err.store(COMPASS_ERR_TIMEOUT); return; }
             _mm_pause();
         }
+    }
+    trace_event(role, job.epoch, "issued", -1, 0);
+    // the job is over once every copy has landed
+    const double t0 = now_s();
+    for (auto sg : issued)
+        while (hsa_signal_load_scacquire(sg) > 0) {
+            if (now_s() - t0 > c.host_timeout) {
+                c.async_err.store(COMPASS_ERR_TIMEOUT);
+                return;
+            }
+            _mm_pause();
+        }
+    if (job.final_flag >= 0) __atomic_store_n(&c.hw[kHwFlags + job.final_flag], job.epoch, __ATOMIC_RELEASE);
+    trace_event(role, job.epoch, "landed", -1, 0);
 }
 
 static void submit(int role, Job &&job) {
@@ -432,21 +496,24 @@ static int take_async_error() {
     return COMPASS_OK;
 }
 
-static uint32_t next_epoch() {
-    Ctx &c = g_ctx;
-    const uint32_t e = ++c.epoch;
-    __atomic_store_n(&c.hw[kHwEpoch + e % kEpochSlots], e, __ATOMIC_RELEASE);
-    return e;
-}
+static uint32_t next_epoch() { return ++g_ctx.epoch; }
 
-static std::vector<uint32_t> engines_for(int role, int roles_active, int per_ring) {
-    const auto &all = g_ctx.engines;
+// SDMA engines of one ring direction: the usable engines are split evenly
+// over the directions active in the operator (`active` lists their roles).
+static std::vector<uint32_t> engines_for(int role, const std::vector<int> &active, int per_ring) {
+    std::vector<uint32_t> all;
+    for (uint32_t e : g_ctx.engines)
+        if (g_ctx.engine_mask == 0 || (g_ctx.engine_mask & e)) all.push_back(e);
+    if (all.empty()) all = g_ctx.engines;
     const int n = (int)all.size();
-    const int share = std::max(1, n / roles_active);
-    int k = per_ring > 0 ? per_ring : std::min(share, roles_active > 2 ? 3 : 4);
-    k = std::min(k, share);
+    const int na = std::max<int>(1, (int)active.size());
+    int pos = 0;
+    for (int i = 0; i < na; ++i)
+        if (active[i] == role) pos = i;
+    const int share = std::max(1, n / na);
+    const int k = per_ring > 0 ? std::min(per_ring, share) : share;
     std::vector<uint32_t> out;
-    for (int i = 0; i < k; ++i) out.push_back(all[(role * share + i) % n]);
+    for (int i = 0; i < k; ++i) out.push_back(all[(pos * share + i) % n]);
     return out;
 }
 
@@ -470,7 +537,7 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     const int P = p->ring == COMPASS_RING_SINGLE ? p->n : 2 * p->n;
     if (p->M % P) return set_error(COMPASS_ERR_INVALID, "M must be divisible by %d", P);
     if (p->K % 8 || p->N % 8) return set_error(COMPASS_ERR_INVALID, "K and N must be multiples of 8");
-    if ((p->M + kTileM - 1) / kTileM > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
+    if ((p->M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
     if ((double)p->M * p->K * 2 >= 2147483648.0 || (double)p->N * p->K * 2 >= 2147483648.0 ||
         (double)p->M * p->N * 4 >= 2147483648.0)
         return set_error(COMPASS_ERR_UNSUPPORTED, "operand larger than 2 GiB");
@@ -501,7 +568,9 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
 static void init_params(GemmParams &g, uint32_t epoch) {
     std::memset(&g, 0, sizeof g);
     Ctx &c = g_ctx;
-    g.flags = c.flags;
+    g.flags = &c.hw[kHwFlags];
+    g.mirror = c.ctrl + kCtrlMirror;
+    g.leader = c.ctrl + kCtrlLeader;
     g.ctrl = c.ctrl;
     g.done_cnt = c.ctrl + kCtrlDone;
     g.err_word = &c.hw[kHwErr];
@@ -509,8 +578,18 @@ static void init_params(GemmParams &g, uint32_t epoch) {
     g.epoch = epoch;
 }
 
-static void set_shape(GemmParams &g, int M, int N, int K, const void *A, size_t a_rows, const void *W, void *C,
-                      const float *P) {
+static int pick_tile(int M, int N, bool gated) {
+    if (g_ctx.tile_override == 1) return kTile256;
+    if (g_ctx.tile_override == 2) return kTile128;
+    // Gated operators need several tiles per arriving partition; a plain GEMM
+    // takes the larger tile when it still fills every CU.
+    if (gated) return kTile128;
+    const long t256 = (long)((M + 255) / 256) * ((N + 255) / 256);
+    return t256 >= g_ctx.num_cu ? kTile256 : kTile128;
+}
+
+static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A, size_t a_rows, const void *W,
+                     void *C, const float *P) {
     g.A = (const uint16_t *)A;
     g.W = (const uint16_t *)W;
     g.C = (uint16_t *)C;
@@ -519,29 +598,53 @@ static void set_shape(GemmParams &g, int M, int N, int K, const void *A, size_t 
     g.lda = K; g.ldw = K; g.ldc = N; g.ldp = N;
     g.a_bytes = (uint32_t)(a_rows * (size_t)K * 2);
     g.w_bytes = (uint32_t)((size_t)N * K * 2);
-    g.tiles_m = (M + kTileM - 1) / kTileM;
-    g.tiles_n = (N + kTileN - 1) / kTileN;
+    const int bm = tile_rows(cfg), bn = tile_cols(cfg);
+    g.tiles_m = (M + bm - 1) / bm;
+    g.tiles_n = (N + bn - 1) / bn;
+    if (g.tiles_m > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large for the tile table");
     const int total = g.tiles_m * g.tiles_n;
-    const int cap = g_ctx.grid_override > 0 ? g_ctx.grid_override : g_ctx.num_cu;
+    const int cap = g_ctx.grid_override > 0 ? g_ctx.grid_override : g_ctx.num_cu * tile_wg_per_cu(cfg);
     g.grid = std::max(1, std::min(total, cap));
-    for (int t = 0; t < g.tiles_m; ++t) g.rt_order[t] = (uint16_t)t;
+    g.nq = g.grid >= kMaxQueues ? kMaxQueues : 1;
+    g.q_size = std::max(1, g.grid / g.nq);
+    g.group_m = cfg == kTile256 ? 4 : 8;
+    for (int t = 0; t < g.tiles_m; ++t) {
+        g.rt_order[t] = (uint16_t)t;
+        g.rt_lo[t] = 0;
+        g.rt_hi[t] = 0;
+    }
+    return COMPASS_OK;
+}
+
+static void touch_all(GemmParams &g, int nparts) {
+    for (int t = 0; t < g.tiles_m; ++t) {
+        g.rt_lo[t] = 0;
+        g.rt_hi[t] = (uint8_t)(nparts - 1);
+    }
 }
 
 // Row tiles ordered by the schedule position of the last partition they
-// touch; touch masks from the identity row map.
-static void order_by_schedule(GemmParams &g, const Geometry &geo, int M) {
+// touch; touched partitions from the identity row map.
+static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M) {
+    const int bm = tile_rows(cfg);
     std::vector<std::pair<int, int>> key;
     for (int t = 0; t < g.tiles_m; ++t) {
-        const int r0 = t * kTileM, r1 = std::min(M, r0 + kTileM) - 1;
+        const int r0 = t * bm, r1 = std::min(M, r0 + bm) - 1;
         const int p0 = r0 / geo.prow, p1 = r1 / geo.prow;
-        uint64_t m = 0;
         int k = 0;
-        for (int q = p0; q <= p1; ++q) { m |= 1ull << q; k = std::max(k, geo.pos[q]); }
-        g.rt_touch[t] = m;
+        for (int q = p0; q <= p1; ++q) k = std::max(k, geo.pos[q]);
+        g.rt_lo[t] = (uint8_t)p0;
+        g.rt_hi[t] = (uint8_t)p1;
         key.push_back({k, t});
     }
     std::stable_sort(key.begin(), key.end());
     for (int i = 0; i < g.tiles_m; ++i) g.rt_order[i] = (uint16_t)key[i].second;
+}
+
+static inline uint64_t touched(const GemmParams &g, int t) {
+    const int lo = g.rt_lo[t], hi = g.rt_hi[t];
+    const uint64_t upto = hi >= 63 ? ~0ull : ((2ull << hi) - 1ull);
+    return upto & ~((1ull << lo) - 1ull);
 }
 
 static hipError_t copy_if_needed(void *dst, const void *src, size_t bytes, hipStream_t s) {
@@ -566,11 +669,11 @@ static int make_item(Item *it, void *dst, const void *src, size_t bytes, int fla
     return COMPASS_OK;
 }
 
-static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, int role, int roles_active) {
+static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, int role, const std::vector<int> &active) {
     j.rate = fwd ? l->fwd_Bps : l->bwd_Bps;
     j.slice = l->slice_bytes ? l->slice_bytes : kDefaultSlice;
     j.epoch = epoch;
-    j.engines = engines_for(role, roles_active, l->engines_per_ring);
+    j.engines = engines_for(role, active, l->engines_per_ring);
 }
 
 // ---------------------------------------------------------------- AllGather jobs
@@ -580,8 +683,9 @@ static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, i
 // with flags j * P + partition.
 static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    bool wait_start, Job *fwd, Job *bwd) {
-    fill_job(*fwd, l, true, epoch, 0, 2);
-    fill_job(*bwd, l, false, epoch, 1, 2);
+    const std::vector<int> active = p->ring == COMPASS_RING_SINGLE ? std::vector<int>{0} : std::vector<int>{0, 1};
+    fill_job(*fwd, l, true, epoch, 0, active);
+    fill_job(*bwd, l, false, epoch, 1, active);
     fwd->wait_start = bwd->wait_start = wait_start;
     const size_t K = (size_t)p->K;
     const int pc = geo.rows / d;                                     // chunk rows per sub-operator
@@ -611,8 +715,14 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
 // on its done flag (or ungated when `gate_out` is false).
 static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    uint64_t resident, bool gate_out, bool wait_start, Job jobs[4]) {
+    std::vector<int> active{0};
+    if (p->ring == COMPASS_RING_DOUBLE) active.push_back(1);
+    if (p->send_dst) {
+        active.push_back(2);
+        if (p->ring == COMPASS_RING_DOUBLE) active.push_back(3);
+    }
     for (int r = 0; r < 4; ++r) {
-        fill_job(jobs[r], l, r % 2 == 0, epoch, r, 4);
+        fill_job(jobs[r], l, r % 2 == 0, epoch, r, active);
         jobs[r].wait_start = wait_start;
     }
     const size_t N = (size_t)p->N;
@@ -689,8 +799,8 @@ static int stage_resident_partials(const compass_problem *p, const Geometry &geo
     return COMPASS_OK;
 }
 
-static int launch(const GemmParams &g, bool rs, hipStream_t s) {
-    const hipError_t e = launch_gemm(g, rs, s);
+static int launch(const GemmParams &g, int cfg, bool rs, hipStream_t s) {
+    const hipError_t e = launch_gemm(g, cfg, rs, s);
     return e == hipSuccess ? COMPASS_OK : hip_fail(e, "GEMM launch");
 }
 
@@ -698,7 +808,7 @@ static int join(uint32_t epoch, const std::vector<int> &flags, bool write_start,
     JoinParams j;
     std::memset(&j, 0, sizeof j);
     Ctx &c = g_ctx;
-    j.flags = c.flags;
+    j.flags = &c.hw[kHwFlags];
     j.start_word = write_start ? &c.hw[kHwStart] : nullptr;
     j.err_word = &c.hw[kHwErr];
     j.epoch = epoch;
@@ -729,15 +839,16 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    set_shape(g, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr);
-    order_by_schedule(g, geo, p->M);
+    const int cfg = pick_tile(p->M, p->N, true);
+    if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
+    order_by_schedule(g, cfg, geo, p->M);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
     g.start_word = &g_ctx.hw[kHwStart];
     submit(0, std::move(fwd));
     submit(1, std::move(bwd));
-    return launch(g, false, s);
+    return launch(g, cfg, false, s);
 }
 
 int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
@@ -753,8 +864,9 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    set_shape(g, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage);
-    order_by_schedule(g, geo, p->M);
+    const int cfg = pick_tile(p->M, p->N, true);
+    if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
+    order_by_schedule(g, cfg, geo, p->M);
     g.gate = kGateEpilogue;
     g.nparts = geo.P;
     g.resident_mask = res;
@@ -767,14 +879,14 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
             if (!(g.send_mask & (1ull << q))) continue;
             uint32_t cnt = 0;
             for (int t = 0; t < g.tiles_m; ++t)
-                if (g.rt_touch[t] & (1ull << q)) cnt += g.tiles_n;
+                if (touched(g, t) & (1ull << q)) cnt += g.tiles_n;
             g.done_expect[q] = cnt;
         }
         for (int r = 2; r < 4; ++r)
             if (jobs[r].final_flag >= 0) finals.push_back(jobs[r].final_flag);
     }
     for (int r = 0; r < 4; ++r) submit(r, std::move(jobs[r]));
-    if ((rc = launch(g, true, s)) != COMPASS_OK) return rc;
+    if ((rc = launch(g, cfg, true, s)) != COMPASS_OK) return rc;
     if (!finals.empty()) return join(epoch, finals, false, s);
     return COMPASS_OK;
 }
@@ -790,7 +902,6 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
     hipStream_t s = (hipStream_t)stream;
     const uint32_t epoch = next_epoch();
     const uint64_t res = resident_mask(p, geo);
-    const uint64_t all = geo.P == 64 ? ~0ull : ((1ull << geo.P) - 1);
     const int piece = geo.rows / d;   // rows of a chunk per sub-operator
     std::vector<int> finals;
     Job ag_f, ag_b, rs[4];
@@ -805,11 +916,14 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
                 if (rs[r].final_flag >= 0) finals.push_back(rs[r].final_flag);
     }
     std::vector<GemmParams> launches(d);
+    const int cfg = pick_tile(p->M / d, p->N, false);
     for (int j = 0; j < d; ++j) {
         GemmParams &g = launches[j];
         init_params(g, epoch);
         const bool ag = p->pattern == COMPASS_AG_GEMM;
-        set_shape(g, p->M / d, p->N, p->K, ag ? p->gathered : p->A, p->M, p->W, p->C, ag ? nullptr : p->partial_stage);
+        if ((rc = set_shape(g, cfg, p->M / d, p->N, p->K, ag ? p->gathered : p->A, p->M, p->W, p->C,
+                            ag ? nullptr : p->partial_stage)) != COMPASS_OK)
+            return rc;
         if (d > 1) {
             g.piece = piece;
             g.pstride = geo.rows;
@@ -819,7 +933,7 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
         g.flag_base = j * geo.P;
         g.nparts = geo.P;
         g.resident_mask = res;
-        for (int t = 0; t < g.tiles_m; ++t) g.rt_touch[t] = all;   // a sub-operator needs its whole sub-collective
+        touch_all(g, geo.P);   // a sub-operator needs its whole sub-collective
         if (j == 0) g.start_word = &g_ctx.hw[kHwStart];
         if (!ag && p->send_dst) {
             g.done_host = &g_ctx.hw[kHwDone];
@@ -835,7 +949,7 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
         for (int r = 0; r < 4; ++r) submit(r, std::move(rs[r]));
     }
     for (int j = 0; j < d; ++j)
-        if ((rc = launch(launches[j], p->pattern == COMPASS_GEMM_RS, s)) != COMPASS_OK) return rc;
+        if ((rc = launch(launches[j], cfg, p->pattern == COMPASS_GEMM_RS, s)) != COMPASS_OK) return rc;
     if (!finals.empty()) return join(epoch, finals, false, s);
     return COMPASS_OK;
 }
@@ -843,16 +957,17 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
 int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream) {
     if (M < 1 || N < 1 || K < 1 || K % 8 || N % 8) return set_error(COMPASS_ERR_INVALID, "need positive M, N, K with K, N multiples of 8");
     if (!A || !W || !C) return set_error(COMPASS_ERR_INVALID, "A, W and C are required");
-    if ((M + kTileM - 1) / kTileM > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
+    if ((M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
     if ((double)M * K * 2 >= 2147483648.0 || (double)N * K * 2 >= 2147483648.0 || (double)M * N * 4 >= 2147483648.0)
         return set_error(COMPASS_ERR_UNSUPPORTED, "operand larger than 2 GiB");
     int rc = begin();
     if (rc != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, g_ctx.epoch);
-    set_shape(g, M, N, K, A, M, W, C, P);
+    const int cfg = pick_tile(M, N, false);
+    if ((rc = set_shape(g, cfg, M, N, K, A, M, W, C, P)) != COMPASS_OK) return rc;
     g.gate = kGateNone;
-    return launch(g, P != nullptr, (hipStream_t)stream);
+    return launch(g, cfg, P != nullptr, (hipStream_t)stream);
 }
 
 int op_transfer(const compass_problem *p, const compass_links *l, void *stream) {
@@ -898,9 +1013,10 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
     if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    set_shape(g, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage);
+    const int cfg = pick_tile(p->M, p->N, false);
+    if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
     g.gate = kGateNone;
-    if ((rc = launch(g, true, s)) != COMPASS_OK) return rc;
+    if ((rc = launch(g, cfg, true, s)) != COMPASS_OK) return rc;
     std::vector<int> wait;
     for (int r = 0; r < 2; ++r)
         for (auto &it : jobs[r].items) wait.push_back(it.flag);
@@ -941,6 +1057,14 @@ int op_set_option(int key, long long v) {
     case COMPASS_OPT_GRID:
         if (v < 0 || v > 65536) return set_error(COMPASS_ERR_INVALID, "grid out of range");
         c.grid_override = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_TILE:
+        if (v < 0 || v > 2) return set_error(COMPASS_ERR_INVALID, "tile option must be 0, 1 or 2");
+        c.tile_override = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_ENGINE_MASK:
+        if (v < 0 || v > 0xFFFF) return set_error(COMPASS_ERR_INVALID, "engine mask out of range");
+        c.engine_mask = (uint32_t)v;
         return COMPASS_OK;
     case COMPASS_OPT_DROP_FLAG:
         if (v < -1 || v >= 2 * kMaxRanks) return set_error(COMPASS_ERR_INVALID, "drop flag out of range");

@@ -268,3 +268,49 @@ def test_invalid_shapes_rejected_before_enqueue():
     st.rank = 7
     with pytest.raises(C.CompassError):
         C.compass_ag_gemm(case.problem, FAST)
+
+
+# ------------------------------------------------------------ both tile configurations
+@pytest.fixture
+def tile_cfg(request):
+    C.compass_set_option(C.OPT_TILE, request.param)
+    yield request.param
+    C.compass_set_option(C.OPT_TILE, 0)
+
+
+@pytest.mark.parametrize("tile_cfg", [1, 2], indirect=True)
+def test_tile_configs_integer_exact(tile_cfg):
+    # plain, fused AllGather, fused ReduceScatter and InterDecom under one tile shape
+    _say("tile cfg", tile_cfg)
+    M, N, K = 1600, 520, 328
+    inp = make_int_ag_inputs(M, N, K, 1, seed=90)
+    A, W = dev_bits(inp["shards"][0]), dev_bits(inp["W"])
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    C.compass_gemm(A, W, Cm)
+    torch.cuda.synchronize()
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"])))
+    assert np.array_equal(host_bits(Cm), ref)
+    n = 8
+    ag = make_int_ag_inputs(2048, 264, 200, n, seed=91)
+    agref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in ag["shards"]], O.bf16_to_f64(ag["W"])))
+    for ring in ["single", "double"]:
+        case = AGCase(ag, 5, ring)
+        C.compass_ag_gemm(case.problem, FAST)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), agref), ring
+        case = AGCase(ag, 2, ring)
+        C.compass_decomp_gemm(case.problem, 4, FAST)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), agref), ring
+    rs = make_int_rs_inputs(2048, 264, 136, n, seed=92)
+    rsref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(rs["A"]), O.bf16_to_f64(rs["W"]),
+                                        [p.astype(np.float64) for p in rs["P_in"]], n))
+    for ring in ["single", "double"]:
+        case = RSCase(rs, 3, ring)
+        C.compass_gemm_rs(case.problem, FAST)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), rsref), ring
+        rows = 2048 // n
+        for q in range(n):
+            if q != 3:
+                assert np.array_equal(host_bits(case.send[q]), rsref[q * rows:(q + 1) * rows])
