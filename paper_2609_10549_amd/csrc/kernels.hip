@@ -138,26 +138,68 @@ __device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rsrc, char *ld
 }
 
 template <int FM, int FN>
-__device__ __forceinline__ void mma_stage(const char *sA, const char *sW, int lane, int wm0, int wn0,
-                                          f32x16 (&acc)[FN][FM]) {
+__device__ __forceinline__ void read_frags(const char *sA, const char *sW, int r, int swz, int kk, int hi,
+                                           int wm0, int wn0, bf16x8 (&a)[FM], bf16x8 (&b)[FN]) {
+    const int coff = ((2 * kk + hi) ^ swz) << 4;
+#pragma unroll
+    for (int mi = 0; mi < FM; ++mi)
+        a[mi] = *reinterpret_cast<const bf16x8 *>(sA + (wm0 + mi * 32 + r) * 128 + coff);
+#pragma unroll
+    for (int ni = 0; ni < FN; ++ni)
+        b[ni] = *reinterpret_cast<const bf16x8 *>(sW + (wn0 + ni * 32 + r) * 128 + coff);
+}
+
+// One K-stage (4 MFMA K-substeps of 16) on the LDS buffers sA/sW. Fragments
+// of substep kk+1 are read from LDS while the MFMAs of kk run (two register
+// sets), and the next stage's global->LDS loads (into dA/dW, when `load`) are
+// spread over the substeps; scheduling groups interleave the three streams.
+template <int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void compute_stage(const char *sA, const char *sW, int lane, int wm0, int wn0,
+                                              f32x16 (&acc)[FN][FM], bool load, __amdgpu_buffer_rsrc_t rA,
+                                              __amdgpu_buffer_rsrc_t rW, char *dA, char *dW,
+                                              const uint32_t *offA, const uint32_t *offW, int cchunk, int k0n,
+                                              int K, int wave) {
+    constexpr int LA = BM / 32, LW = BN / 32;           // global loads per wave per stage
+    constexpr int LAK = LA / 4, LWK = LW / 4;           // ... per substep
     const int r = lane & 31;
     const int swz = (r >> 1) & 7;
+    const int hi = lane >> 5;
+    const int kc = k0n + cchunk * 8;
+    const bool kin = kc < K;
+    bf16x8 a[2][FM], b[2][FN];
+    read_frags<FM, FN>(sA, sW, r, swz, 0, hi, wm0, wn0, a[0], b[0]);
 #pragma unroll
     for (int kk = 0; kk < kTileK / 16; ++kk) {
-        const int c = 2 * kk + (lane >> 5);
-        const int coff = (c ^ swz) << 4;
-        bf16x8 a[FM], b[FN];
+        const int cur = kk & 1;
+        if (kk + 1 < kTileK / 16) read_frags<FM, FN>(sA, sW, r, swz, kk + 1, hi, wm0, wn0, a[cur ^ 1], b[cur ^ 1]);
+        if (load) {
 #pragma unroll
-        for (int mi = 0; mi < FM; ++mi)
-            a[mi] = *reinterpret_cast<const bf16x8 *>(sA + (wm0 + mi * 32 + r) * 128 + coff);
+            for (int j = 0; j < LAK; ++j) {
+                const int q = kk * LAK + j;
+                const uint32_t off = (offA[q] == kOOB || !kin) ? kOOB : offA[q] + (uint32_t)kc * 2u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, LDS_AS(dA + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
+            }
 #pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-            b[ni] = *reinterpret_cast<const bf16x8 *>(sW + (wn0 + ni * 32 + r) * 128 + coff);
+            for (int j = 0; j < LWK; ++j) {
+                const int q = kk * LWK + j;
+                const uint32_t off = (offW[q] == kOOB || !kin) ? kOOB : offW[q] + (uint32_t)kc * 2u;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, LDS_AS(dW + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
+            }
+        }
 #pragma unroll
         for (int ni = 0; ni < FN; ++ni)
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi)
-                acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ni], a[mi], acc[ni][mi], 0, 0, 0);
+                acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][ni], a[cur][mi], acc[ni][mi], 0, 0, 0);
+        // per substep: FM*FN MFMAs, FM+FN LDS reads (next substep), LAK+LWK
+        // global loads; alternate MFMA with reads and loads
+        constexpr int NM = FM * FN, ND = FM + FN, NV = LAK + LWK;
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+            if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+        }
     }
 }
 
@@ -254,16 +296,12 @@ void gemm_kernel(const GemmParams p) {
             for (int kt = 0; kt < KT2; kt += 2) {
                 __builtin_amdgcn_s_waitcnt(0);
                 __syncthreads();
-                load_stage<BM>(rA, sA1, offA, cchunk, (kt + 1) * kTileK, p.K, wave);
-                load_stage<BN>(rW, sW1, offW, cchunk, (kt + 1) * kTileK, p.K, wave);
-                mma_stage<FM, FN>(sA0, sW0, lane, wm0, wn0, acc);
+                compute_stage<BM, BN, FM, FN>(sA0, sW0, lane, wm0, wn0, acc, true, rA, rW, sA1, sW1, offA, offW,
+                                              cchunk, (kt + 1) * kTileK, p.K, wave);
                 __builtin_amdgcn_s_waitcnt(0);
                 __syncthreads();
-                if (kt + 2 < KT2) {
-                    load_stage<BM>(rA, sA0, offA, cchunk, (kt + 2) * kTileK, p.K, wave);
-                    load_stage<BN>(rW, sW0, offW, cchunk, (kt + 2) * kTileK, p.K, wave);
-                }
-                mma_stage<FM, FN>(sA1, sW1, lane, wm0, wn0, acc);
+                compute_stage<BM, BN, FM, FN>(sA1, sW1, lane, wm0, wn0, acc, kt + 2 < KT2, rA, rW, sA0, sW0, offA,
+                                              offW, cchunk, (kt + 2) * kTileK, p.K, wave);
             }
         }
 

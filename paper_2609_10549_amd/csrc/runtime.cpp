@@ -72,7 +72,7 @@ static double now_s() {
 // ---------------------------------------------------------------- state
 constexpr int kRoles = 4;            // in-fwd, in-bwd, out-fwd, out-bwd
 constexpr int kSignals = 256;        // completion signals per pacer
-constexpr size_t kDefaultSlice = 4u << 20;
+constexpr size_t kDefaultSlice = 2u << 20;
 // host_words layout (pinned, coherent host memory): start word, error word,
 // done flags (kernel -> copy side), arrival flags (copy side -> kernel)
 constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
@@ -500,20 +500,32 @@ static uint32_t next_epoch() { return ++g_ctx.epoch; }
 
 // SDMA engines of one ring direction: the usable engines are split evenly
 // over the directions active in the operator (`active` lists their roles).
-static std::vector<uint32_t> engines_for(int role, const std::vector<int> &active, int per_ring) {
+// SDMA engines of one ring direction: the usable engines are split over the
+// directions active in the operator in proportion to the bytes each carries
+// (`active` lists their roles, `weight` their relative traffic).
+static std::vector<uint32_t> engines_for(int role, const std::vector<int> &active, const std::vector<int> &weight,
+                                         int per_ring) {
     std::vector<uint32_t> all;
     for (uint32_t e : g_ctx.engines)
         if (g_ctx.engine_mask == 0 || (g_ctx.engine_mask & e)) all.push_back(e);
     if (all.empty()) all = g_ctx.engines;
     const int n = (int)all.size();
     const int na = std::max<int>(1, (int)active.size());
-    int pos = 0;
-    for (int i = 0; i < na; ++i)
-        if (active[i] == role) pos = i;
-    const int share = std::max(1, n / na);
-    const int k = per_ring > 0 ? std::min(per_ring, share) : share;
+    int wsum = 0;
+    for (int i = 0; i < na; ++i) wsum += weight[i];
+    int first = 0, count = 1;
+    for (int i = 0, acc = 0; i < na; ++i) {
+        const int lo = (int)((long)n * acc / wsum);
+        acc += weight[i];
+        const int hi = (int)((long)n * acc / wsum);
+        if (active[i] == role) {
+            first = lo;
+            count = std::max(1, hi - lo);
+        }
+    }
+    if (per_ring > 0) count = std::min(count, per_ring);
     std::vector<uint32_t> out;
-    for (int i = 0; i < k; ++i) out.push_back(all[(pos * share + i) % n]);
+    for (int i = 0; i < count; ++i) out.push_back(all[(first + i) % n]);
     return out;
 }
 
@@ -669,11 +681,12 @@ static int make_item(Item *it, void *dst, const void *src, size_t bytes, int fla
     return COMPASS_OK;
 }
 
-static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, int role, const std::vector<int> &active) {
+static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, int role, const std::vector<int> &active,
+                     const std::vector<int> &weight) {
     j.rate = fwd ? l->fwd_Bps : l->bwd_Bps;
     j.slice = l->slice_bytes ? l->slice_bytes : kDefaultSlice;
     j.epoch = epoch;
-    j.engines = engines_for(role, active, l->engines_per_ring);
+    j.engines = engines_for(role, active, weight, l->engines_per_ring);
 }
 
 // ---------------------------------------------------------------- AllGather jobs
@@ -684,8 +697,9 @@ static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, i
 static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    bool wait_start, Job *fwd, Job *bwd) {
     const std::vector<int> active = p->ring == COMPASS_RING_SINGLE ? std::vector<int>{0} : std::vector<int>{0, 1};
-    fill_job(*fwd, l, true, epoch, 0, active);
-    fill_job(*bwd, l, false, epoch, 1, active);
+    const std::vector<int> weight(active.size(), 1);
+    fill_job(*fwd, l, true, epoch, 0, active, weight);
+    fill_job(*bwd, l, false, epoch, 1, active, weight);
     fwd->wait_start = bwd->wait_start = wait_start;
     const size_t K = (size_t)p->K;
     const int pc = geo.rows / d;                                     // chunk rows per sub-operator
@@ -715,14 +729,15 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
 // on its done flag (or ungated when `gate_out` is false).
 static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    uint64_t resident, bool gate_out, bool wait_start, Job jobs[4]) {
-    std::vector<int> active{0};
-    if (p->ring == COMPASS_RING_DOUBLE) active.push_back(1);
+    // incoming fp32 partials carry twice the bytes of the outgoing bf16 sums
+    std::vector<int> active{0}, weight{2};
+    if (p->ring == COMPASS_RING_DOUBLE) { active.push_back(1); weight.push_back(2); }
     if (p->send_dst) {
-        active.push_back(2);
-        if (p->ring == COMPASS_RING_DOUBLE) active.push_back(3);
+        active.push_back(2); weight.push_back(1);
+        if (p->ring == COMPASS_RING_DOUBLE) { active.push_back(3); weight.push_back(1); }
     }
     for (int r = 0; r < 4; ++r) {
-        fill_job(jobs[r], l, r % 2 == 0, epoch, r, active);
+        fill_job(jobs[r], l, r % 2 == 0, epoch, r, active, weight);
         jobs[r].wait_start = wait_start;
     }
     const size_t N = (size_t)p->N;
