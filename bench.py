@@ -155,6 +155,7 @@ def main():
         step()
     C.compass_sync()
     torch.cuda.synchronize()
+    C.compass_set_option(C.OPT_KERNEL_TIMING, 1)   # HIP events around every GEMM launch
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     say(f"bench: timing {args.steps} steps")
     torch.cuda.synchronize()
@@ -168,20 +169,31 @@ def main():
     torch.cuda.synchronize()
     C.compass_sync()
     wall = time.perf_counter() - t0
+    kt = C.compass_kernel_times(4 * args.steps * 32)
+    C.compass_set_option(C.OPT_KERNEL_TIMING, 0)
     op1 = [ev[k][0].elapsed_time(ev[k][1]) * 1e-3 for k in range(args.steps)]
     op2 = [ev[k][1].elapsed_time(ev[k][2]) * 1e-3 for k in range(args.steps)]
     ms_per_step = wall / args.steps * 1e3
     t_op1, t_op2 = float(np.mean(op1)), float(np.mean(op2))
     value = (flops1 + flops2) / (wall / args.steps) / 1e12
 
-    # dominant kernel: the GEMM kernel of the longer operator
-    if t_op1 >= t_op2:
-        dom = dict(name=f"gemm_kernel<AllGather> ({s1})", flops=flops1, t=t_op1)
+    # dominant kernel: the GEMM launches with the larger total time; each
+    # step launches d1 kernels for fc1, then d2 for fc2
+    per = d1 + d2
+    done = len(kt) // per              # the runtime records at most 512 launches
+    assert done >= 1, (len(kt), per)
+    k1 = [kt[i * per + j] for i in range(done) for j in range(d1)]
+    k2 = [kt[i * per + d1 + j] for i in range(done) for j in range(d2)]
+    if sum(k1) >= sum(k2):
+        dom = dict(name=f"gemm_kernel, fc1 AllGather ({s1}, d={d1})", flops=flops1 / d1, t=float(np.mean(k1)) * 1e-6,
+                   tag="ag")
     else:
-        dom = dict(name=f"gemm_kernel<ReduceScatter> ({s2}, incl. send join)", flops=flops2, t=t_op2)
+        dom = dict(name=f"gemm_kernel, fc2 ReduceScatter ({s2}, d={d2})", flops=flops2 / d2,
+                   t=float(np.mean(k2)) * 1e-6, tag="rs")
     achieved = dom["flops"] / dom["t"] / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom["name"]}
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": stored_traffic(dom["tag"]),
+                "kernel": dom["name"], "kernel_us": round(dom["t"] * 1e6, 2)}
 
     result = {
         "metric": "AG-GEMM/GEMM-RS TFLOP/s + overlap efficiency vs unfused GEMM+copy, 1 GPU",
@@ -239,6 +251,21 @@ def main():
         say("bench: CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(ag_in, rs_in)
     print(json.dumps(result))
+
+
+def stored_traffic(tag):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    runs (profiles/traffic_<tag>.json), or None when absent or taken with a
+    different kernel source."""
+    from paper_2609_10549_amd import profile_summary as PS
+    path = os.path.join(ROOT, "profiles", f"traffic_{tag}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_hash") != PS.kernel_source_hash():
+        return None
+    return round(rec["traffic_bytes_per_launch"], 0)
 
 
 def cpu_baseline(ag_in, rs_in) -> dict:

@@ -81,7 +81,7 @@ int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int c
  * Rates are the emulated per-direction link bandwidths of the two rings
  * (bytes per second). A single ring uses fwd_Bps only. A rate <= 0 means
  * "unpaced" (copies go out as fast as the engines take them). Copies are
- * issued in slices of `slice_bytes` (0: library default, 4 MiB), each slice
+ * issued in slices of `slice_bytes` (0: library default, 2 MiB), each slice
  * no earlier than its paced time, striped over `engines_per_ring` SDMA
  * engines (0: library default). */
 typedef struct compass_links {
@@ -197,7 +197,16 @@ int compass_sync(void);
                                        (one workgroup per CU), 2 = 128 x 128 (two) */
 #define COMPASS_OPT_ENGINE_MASK  6  /* bit i set: SDMA engine i may carry emulated link
                                        traffic; 0 = every engine that accepts a copy */
+#define COMPASS_OPT_KERNEL_TIMING 7 /* 1: record HIP events on the launch stream around
+                                       every GEMM kernel (up to 512 between reads) */
 int compass_set_option(int key, long long value);
+
+/* Durations in microseconds of the GEMM kernels launched since the previous
+ * call (launch order), measured with HIP events recorded on their stream
+ * right before and after each launch; waits for those events. Needs
+ * COMPASS_OPT_KERNEL_TIMING = 1. Writes at most `cap` values and returns the
+ * number written, or a negative status. */
+int compass_kernel_times(double *us, int cap);
 
 /* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */
 typedef struct compass_workload {   /* W of Eq. 1 / Eq. 6 */

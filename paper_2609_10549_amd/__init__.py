@@ -12,6 +12,7 @@ from .compass import (  # noqa: F401
     compass_decomp_gemm,
     compass_gemm,
     compass_gemm_rs,
+    compass_kernel_times,
     compass_last_error,
     compass_model_t_decomp,
     compass_model_t_fusion,

@@ -33,6 +33,7 @@ OPT_GRID = 3
 OPT_DROP_FLAG = 4
 OPT_TILE = 5
 OPT_ENGINE_MASK = 6
+OPT_KERNEL_TIMING = 7
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE}
@@ -103,6 +104,7 @@ _SIGS = {
     "compass_transfer": (ctypes.c_int, [ctypes.POINTER(compass_problem), ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_sequential": (ctypes.c_int, [ctypes.POINTER(compass_problem), ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_sync": (ctypes.c_int, []),
+    "compass_kernel_times": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
     "compass_set_option": (ctypes.c_int, [ctypes.c_int, ctypes.c_longlong]),
     "compass_pick_strategy": (ctypes.c_int, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology),
                                              ctypes.POINTER(compass_calib), ctypes.POINTER(compass_choice)]),
@@ -251,6 +253,12 @@ def compass_sequential(problem: Problem, lk: compass_links | None = None, stream
 
 def compass_sync() -> None:
     _check(lib().compass_sync(), "compass_sync")
+
+
+def compass_kernel_times(cap: int = 512) -> list:
+    out = (ctypes.c_double * cap)()
+    k = _check(lib().compass_kernel_times(out, cap), "compass_kernel_times")
+    return list(out[:k])
 
 
 def compass_set_option(key: int, value: int) -> None:

@@ -26,5 +26,6 @@ int op_transfer(const compass_problem *p, const compass_links *l, void *stream);
 int op_sequential(const compass_problem *p, const compass_links *l, void *stream);
 int op_sync();
 int op_set_option(int key, long long value);
+int op_kernel_times(double *us, int cap);
 
 }  // namespace compass

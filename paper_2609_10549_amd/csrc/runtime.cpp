@@ -136,6 +136,11 @@ struct Ctx {
     int grid_override = 0;
     int drop_flag = -1;
     int tile_override = 0;           // 0 auto, 1 256 x 256, 2 128 x 128
+    // optional HIP events around every GEMM launch (kernel durations)
+    bool timing = false;
+    static constexpr int kTimed = 512;
+    hipEvent_t ev_begin[kTimed] = {}, ev_end[kTimed] = {};
+    int timed_count = 0;             // launches recorded since the last read
     uint32_t engine_mask = 0;        // hardware engines allowed (0: all usable)
     // copy-side trace (COMPASS_TRACE=<file>): one line per event
     bool tracing = false;
@@ -815,8 +820,29 @@ static int stage_resident_partials(const compass_problem *p, const Geometry &geo
 }
 
 static int launch(const GemmParams &g, int cfg, bool rs, hipStream_t s) {
+    Ctx &c = g_ctx;
+    const bool timed = c.timing && c.timed_count < Ctx::kTimed;
+    if (timed) hipEventRecord(c.ev_begin[c.timed_count], s);
     const hipError_t e = launch_gemm(g, cfg, rs, s);
-    return e == hipSuccess ? COMPASS_OK : hip_fail(e, "GEMM launch");
+    if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+    if (timed) hipEventRecord(c.ev_end[c.timed_count++], s);
+    return COMPASS_OK;
+}
+
+int op_kernel_times(double *us, int cap) {
+    Ctx &c = g_ctx;
+    if (!c.ready || !c.timing) return set_error(COMPASS_ERR_INVALID, "kernel timing is not enabled");
+    if (cap < 0 || (cap > 0 && !us)) return set_error(COMPASS_ERR_INVALID, "bad output buffer");
+    const int n = std::min(cap, c.timed_count);
+    for (int i = 0; i < n; ++i) {
+        float ms = 0.f;
+        hipError_t e = hipEventSynchronize(c.ev_end[i]);
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, c.ev_begin[i], c.ev_end[i]);
+        if (e != hipSuccess) return hip_fail(e, "kernel event");
+        us[i] = (double)ms * 1e3;
+    }
+    c.timed_count = 0;
+    return n;
 }
 
 static int join(uint32_t epoch, const std::vector<int> &flags, bool write_start, hipStream_t s) {
@@ -1081,6 +1107,22 @@ int op_set_option(int key, long long v) {
         if (v < 0 || v > 0xFFFF) return set_error(COMPASS_ERR_INVALID, "engine mask out of range");
         c.engine_mask = (uint32_t)v;
         return COMPASS_OK;
+    case COMPASS_OPT_KERNEL_TIMING: {
+        if (v != 0 && v != 1) return set_error(COMPASS_ERR_INVALID, "kernel timing option must be 0 or 1");
+        if (v == 1 && !c.timing) {
+            const int rc = ensure_init();
+            if (rc != COMPASS_OK) return rc;
+            for (int i = 0; i < Ctx::kTimed; ++i) {
+                if (!c.ev_begin[i] && hipEventCreate(&c.ev_begin[i]) != hipSuccess)
+                    return set_error(COMPASS_ERR_HIP, "hipEventCreate failed");
+                if (!c.ev_end[i] && hipEventCreate(&c.ev_end[i]) != hipSuccess)
+                    return set_error(COMPASS_ERR_HIP, "hipEventCreate failed");
+            }
+        }
+        c.timing = v == 1;
+        c.timed_count = 0;
+        return COMPASS_OK;
+    }
     case COMPASS_OPT_DROP_FLAG:
         if (v < -1 || v >= 2 * kMaxRanks) return set_error(COMPASS_ERR_INVALID, "drop flag out of range");
         c.drop_flag = (int)v;

@@ -314,3 +314,28 @@ def test_tile_configs_integer_exact(tile_cfg):
         for q in range(n):
             if q != 3:
                 assert np.array_equal(host_bits(case.send[q]), rsref[q * rows:(q + 1) * rows])
+
+
+# ------------------------------------------------------------ per-launch kernel timing
+def test_kernel_times_one_per_launch():
+    _say("kernel times")
+    M, N, K = 1024, 512, 256
+    inp = make_int_ag_inputs(M, N, K, 1, seed=93)
+    A, W = dev_bits(inp["shards"][0]), dev_bits(inp["W"])
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    with pytest.raises(C.CompassError):
+        C.compass_kernel_times()          # not enabled
+    C.compass_set_option(C.OPT_KERNEL_TIMING, 1)
+    try:
+        C.compass_gemm(A, W, Cm)
+        C.compass_gemm(A, W, Cm)
+        ag = make_int_ag_inputs(2048, 264, 200, 8, seed=94)
+        case = AGCase(ag, 1, "double")
+        C.compass_decomp_gemm(case.problem, 4, FAST)
+        C.compass_sync()
+        t = C.compass_kernel_times()
+        assert len(t) == 2 + 4
+        assert all(0.0 < x < 1e6 for x in t)
+        assert C.compass_kernel_times() == []   # reading resets
+    finally:
+        C.compass_set_option(C.OPT_KERNEL_TIMING, 0)
