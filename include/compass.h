@@ -79,11 +79,23 @@ int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int c
 
 /* ---- emulated links -----------------------------------------------------
  * Rates are the emulated per-direction link bandwidths of the two rings
- * (bytes per second). A single ring uses fwd_Bps only. A rate <= 0 means
- * "unpaced" (copies go out as fast as the engines take them). Copies are
- * issued in slices of `slice_bytes` (0: library default, 2 MiB), each slice
- * no earlier than its paced time, striped over `engines_per_ring` SDMA
- * engines (0: library default). */
+ * (bytes per second). A single ring uses fwd_Bps only.
+ *
+ * Paced (rate >= 1e8): the link delivers one item (a partition, or a chunk
+ * sum sent onward) at a time at that rate; an item is due when the link has
+ * finished the previous one (or its data became ready, if later) plus
+ * bytes / rate. Its arrival flag is never published before the due time.
+ * The copy goes out whole on a group of the ring direction's SDMA engines,
+ * ahead of its due time by its predicted latency; if the engines cannot
+ * keep up, items arrive late (the achieved rate is what transfer timings
+ * measure).
+ * Unpaced (rate <= 0): copies go out as fast as the engines take them, in
+ * slices round-robin over the engines; flags publish when the data landed.
+ * Rates in (0, 1e8) are rejected.
+ *
+ * slice_bytes: largest single copy (0: library default, 2 MiB; else
+ * >= 4 KiB). engines_per_ring: SDMA engines per ring direction (0: library
+ * default, all usable engines split over the active directions). */
 typedef struct compass_links {
     double fwd_Bps;
     double bwd_Bps;
@@ -96,8 +108,8 @@ typedef struct compass_links {
  * The emulated rank r owns row chunk r, rows [r*M/n, (r+1)*M/n).
  *
  * Requirements: 1 <= n <= 32, 0 <= rank < n, M % n == 0 (and M % (2n) == 0
- * for the double ring), K % 8 == 0, N % 8 == 0, M*K*2, N*K*2 and M*N*4 below
- * 2^31 bytes, M / 256 rounded up at most 512.
+ * for the double ring), K % 8 == 0, N % 8 == 0, M*K*2 and N*K*2 at most
+ * 2^30 bytes, M*N*4 below 2^31 bytes, M / 128 rounded up at most 512.
  *
  * AllGather + GEMM (pattern COMPASS_AG_GEMM):
  *   shard_src[q], q = 0..n-1: (M/n) x K bf16 shard of rank q. shard_src[rank]
@@ -169,7 +181,8 @@ int compass_decomp_gemm(const compass_problem *p, int d, const compass_links *li
 /* ---- measurement companions ----------------------------------------------
  * compass_gemm: the same GEMM kernel with nothing to wait for (T_gemm).
  *   A: device M x K bf16, W: device N x K bf16, C: device M x N bf16,
- *   P: NULL or device M x N fp32 added before rounding.
+ *   P: NULL or device M x N fp32 added before rounding. Same size limits as
+ *   a compass_problem (K, N multiples of 8; A and W at most 1 GiB).
  * compass_transfer: exactly the copies the fused operator of `p` issues, at
  *   the same pacing, with no GEMM (T_xfer); a one-workgroup kernel on the
  *   stream starts the copies and ends when the last one landed.
@@ -199,6 +212,12 @@ int compass_sync(void);
                                        traffic; 0 = every engine that accepts a copy */
 #define COMPASS_OPT_KERNEL_TIMING 7 /* 1: record HIP events on the launch stream around
                                        every GEMM kernel (up to 512 between reads) */
+#define COMPASS_OPT_TILE_TRACE   8  /* > 0: record one timing record per output tile of
+                                       every GEMM launch, up to this many records
+                                       (a device buffer of value * 32 bytes); 0 = off */
+#define COMPASS_OPT_SCHED        9  /* tile dealing of gated operators, bit mask (default 3):
+                                       1 = super-blocks of one row-tile group per XCD
+                                       queue, 2 = first tickets spread one per CU */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous
@@ -207,6 +226,18 @@ int compass_set_option(int key, long long value);
  * COMPASS_OPT_KERNEL_TIMING = 1. Writes at most `cap` values and returns the
  * number written, or a negative status. */
 int compass_kernel_times(double *us, int cap);
+
+/* Tile records of the GEMM launches since the previous call (tracing aid for
+ * the overlap analysis; needs COMPASS_OPT_TILE_TRACE > 0). Synchronizes the
+ * device, copies at most `cap` records of 8 uint32 each into host memory
+ * `records` (caller-owned, 32 * cap bytes) and returns the number copied, or
+ * a negative status. Records are in launch order, one block of
+ * tiles_m * tiles_n records per launch, indexed by the tile's position in the
+ * launch's ready order: [0] position, [1] row tile << 16 | column tile,
+ * [2] HW_ID and [3] XCC_ID of the workgroup that ran it, [4..7] the GPU's
+ * 100 MHz real-time counter (low 32 bits) when the workgroup took the ticket,
+ * passed the arrival gate, left the main loop and finished the epilogue. */
+int compass_tile_trace(uint32_t *records, int cap);
 
 /* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */
 typedef struct compass_workload {   /* W of Eq. 1 / Eq. 6 */

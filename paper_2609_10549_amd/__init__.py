@@ -13,6 +13,7 @@ from .compass import (  # noqa: F401
     compass_gemm,
     compass_gemm_rs,
     compass_kernel_times,
+    compass_tile_trace,
     compass_last_error,
     compass_model_t_decomp,
     compass_model_t_fusion,

@@ -34,6 +34,8 @@ OPT_DROP_FLAG = 4
 OPT_TILE = 5
 OPT_ENGINE_MASK = 6
 OPT_KERNEL_TIMING = 7
+OPT_TILE_TRACE = 8
+OPT_SCHED = 9
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE}
@@ -105,6 +107,7 @@ _SIGS = {
     "compass_sequential": (ctypes.c_int, [ctypes.POINTER(compass_problem), ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_sync": (ctypes.c_int, []),
     "compass_kernel_times": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
+    "compass_tile_trace": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint32), ctypes.c_int]),
     "compass_set_option": (ctypes.c_int, [ctypes.c_int, ctypes.c_longlong]),
     "compass_pick_strategy": (ctypes.c_int, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology),
                                              ctypes.POINTER(compass_calib), ctypes.POINTER(compass_choice)]),
@@ -259,6 +262,16 @@ def compass_kernel_times(cap: int = 512) -> list:
     out = (ctypes.c_double * cap)()
     k = _check(lib().compass_kernel_times(out, cap), "compass_kernel_times")
     return list(out[:k])
+
+
+def compass_tile_trace(cap: int = 1 << 16):
+    """Tile records (numpy uint32, shape (k, 8)) of the GEMM launches since the
+    previous call; see the header for the fields."""
+    import numpy as np
+    out = np.zeros((cap, 8), dtype=np.uint32)
+    k = _check(lib().compass_tile_trace(out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), cap),
+               "compass_tile_trace")
+    return out[:k]
 
 
 def compass_set_option(key: int, value: int) -> None:

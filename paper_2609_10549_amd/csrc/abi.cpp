@@ -40,6 +40,8 @@ int compass_set_option(int key, long long value) { return op_set_option(key, val
 
 int compass_kernel_times(double *us, int cap) { return op_kernel_times(us, cap); }
 
+int compass_tile_trace(uint32_t *records, int cap) { return op_tile_trace(records, cap); }
+
 int compass_pick_strategy(const compass_workload *w, const compass_topology *t, const compass_calib *cal,
                           compass_choice *out) {
     return pick(w, t, cal, out);

@@ -27,5 +27,6 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
 int op_sync();
 int op_set_option(int key, long long value);
 int op_kernel_times(double *us, int cap);
+int op_tile_trace(uint32_t *out, int cap);
 
 }  // namespace compass

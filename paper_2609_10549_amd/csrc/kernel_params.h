@@ -4,7 +4,6 @@
 
 namespace compass {
 
-constexpr int kTileK = 64;           // K depth of one LDS stage
 constexpr int kThreads = 256;        // 4 waves of 64, 2 x 2 over the tile
 constexpr int kMaxRowTiles = 512;    // row tiles per launch
 constexpr int kMaxParts = 64;        // partitions per launch (2 n, n <= 32)
@@ -13,6 +12,8 @@ constexpr int kFinalFlag0 = kMaxFlags - 8;  // end-of-job flags
 constexpr int kMaxJoin = 80;
 constexpr int kMaxQueues = 8;        // ticket queues (one per XCD)
 constexpr int kCtrlExit = kMaxQueues;       // ctrl word: exit counter
+constexpr int kTraceWords = 8;       // words per tile-trace record
+constexpr int kCuSlots = 8 * 256;    // ctrl words: per (XCC, SE/SH/CU id) slot claims
 
 // Tile configurations of the GEMM kernel.
 enum TileCfg : int {
@@ -48,6 +49,13 @@ struct GemmParams {
     // positions walk group_m row tiles before the next column tile
     int nq, q_size, group_m;
     int grid;
+    // first-ticket spreading: the second workgroup on a CU (by HW_ID) takes
+    // its first ticket only once `spread_wait` tickets of its queue are gone
+    // (or after ~10 us), so the first tickets land one per CU; 0 = off.
+    // `cu_slots` are claim words tagged with `launch_seq`.
+    int spread_wait;
+    uint32_t launch_seq;
+    uint32_t *cu_slots;
     // gating: flag index of partition p is flag_base + p. Arrival flags live
     // in pinned host memory (written by the copy-side threads); the first
     // workgroup that needs a partition in an epoch (`leader`) polls it and
@@ -69,6 +77,12 @@ struct GemmParams {
     uint32_t *ctrl;          // [0, nq) tickets, [kCtrlExit] exit counter
     uint32_t *start_word;    // host-visible; written with epoch at start (or null)
     uint32_t *err_word;      // host-visible error word
+    // optional tile trace: record (trace_base + position) gets kTraceWords
+    // words: position, row tile << 16 | column tile, HW_ID, XCC_ID, and the
+    // 100 MHz real-time counter (low 32 bits) at ticket, after the gate, after
+    // the main loop and after the epilogue
+    uint32_t *tile_trace;
+    uint32_t trace_base, trace_cap;
     uint16_t rt_order[kMaxRowTiles];   // ready order of the row tiles
     uint8_t rt_lo[kMaxRowTiles];       // partitions [lo, hi] a row tile depends on
     uint8_t rt_hi[kMaxRowTiles];

@@ -15,13 +15,21 @@
 // column tile, so the tiles one XCD holds at a time share A rows and W rows
 // in that XCD's L2.
 //
-// Data path per tile: A and W stream through LDS in K-steps of 64, double
-// buffered; global -> LDS moves use buffer_load ... lds (no register staging;
-// out-of-range rows or K columns read as zero through the buffer bound). The
-// 4 waves split the tile 2 x 2; each wave holds (BM/2) x (BN/2) fp32
-// accumulators as 32 x 32 MFMA blocks. LDS rows are 128 bytes; the 16-byte
-// chunks of row r are XOR-permuted with (r >> 1) & 7 so that a fragment read
-// (32 rows, one chunk) hits distinct banks.
+// Data path per tile: 4 waves split the tile 2 x 2; each wave holds
+// (BM/2) x (BN/2) fp32 accumulators as 32 x 32 MFMA blocks. A and W stream
+// through LDS with buffer_load ... lds (no register staging; out-of-range
+// rows or K columns read as zero through the buffer bound). Fragment reads
+// of the next MFMA substep are issued between the MFMAs of the current one,
+// and scheduling barriers keep the compiler from sinking them to their use.
+//   256 x 256 (one workgroup per CU): four LDS stages of K = 32 (rows of 64
+//   bytes, 16-byte chunks of row r XOR-permuted by (r >> 2) & 3); loads run
+//   three stages ahead, and the one barrier per stage sits before the last
+//   substep, so the next stage's first fragments are read while that substep
+//   computes.
+//   128 x 128 (two workgroups per CU): two LDS stages of K = 64 (rows of 128
+//   bytes, chunks permuted by (r >> 1) & 7); the next stage's loads go out
+//   in the first two substeps.
+// Either permutation makes a 32-row fragment read hit distinct banks.
 //
 // join_kernel: one wave that (optionally) marks the start of a transfer job
 // and waits for a list of flags, putting the end of the copy side onto the
@@ -39,7 +47,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_AS(p) ((__attribute__((address_space(3))) void *)(p))
 
-constexpr uint32_t kOOB = 0x80000000u;   // byte offset beyond every buffer bound
+// Offset added for an out-of-range row or K column: A and W are at most
+// 1 GiB each, so a row offset plus a column offset (either possibly kOOB)
+// stays below 2^32 and lands beyond the buffer bound whenever either is kOOB.
+constexpr uint32_t kOOB = 0x40000000u;
 
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -97,6 +108,39 @@ __device__ bool wait_flags(const GemmParams &p, uint64_t mask) {
     return true;
 }
 
+__device__ __forceinline__ uint32_t rtc32() { return (uint32_t)__builtin_amdgcn_s_memrealtime(); }
+
+__device__ __forceinline__ uint32_t hw_id() {
+    uint32_t v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(v));
+    return v;
+}
+
+__device__ __forceinline__ uint32_t xcc_id() {
+    uint32_t v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+    return v;
+}
+
+// Order of this workgroup among the workgroups of this launch on its CU
+// (0 for the first): a claim word per (XCC, SE, SH, CU) holds
+// launch_seq << 8 | count.
+__device__ uint32_t claim_cu_slot(const GemmParams &p) {
+    const uint32_t key = ((xcc_id() & 7u) << 8) | ((hw_id() >> 8) & 0xFFu);
+    uint32_t *w = p.cu_slots + key;
+    const uint32_t tag = p.launch_seq & 0xFFFFFFu;
+    uint32_t cur = ld_dev(w);
+    for (;;) {
+        const bool same = (cur >> 8) == tag;
+        const uint32_t want = same ? cur + 1u : ((tag << 8) | 1u);
+        uint32_t expect = cur;
+        if (__hip_atomic_compare_exchange_strong(w, &expect, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT))
+            return same ? (cur & 0xFFu) : 0u;
+        cur = expect;
+    }
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     const __bf16 a = (__bf16)lo, b = (__bf16)hi;   // round to nearest even
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
@@ -120,87 +164,144 @@ __device__ __forceinline__ int ticket_position(const GemmParams &p, int v, uint3
     return (v + p.nq * k) * p.q_size + i;
 }
 
-// Issue one K-stage (64 columns) of an R-row operand into LDS. Load q of a
-// wave fills LDS bytes [(4q + wave) KiB, +1 KiB): rows 32q + 8 wave + lane/8,
-// physical chunk lane % 8, which holds logical chunk `cchunk` (the XOR
-// permutation; one value per lane). `row_off` is each load's row start in
-// bytes, kOOB past the last row.
-template <int R>
-__device__ __forceinline__ void load_stage(__amdgpu_buffer_rsrc_t rsrc, char *lds, const uint32_t *row_off,
-                                           int cchunk, int k0, int K, int wave) {
-    const int kc = k0 + cchunk * 8;
-    const bool kin = kc < K;
-#pragma unroll
-    for (int q = 0; q < R / 32; ++q) {
-        const uint32_t off = (row_off[q] == kOOB || !kin) ? kOOB : row_off[q] + (uint32_t)kc * 2u;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_AS(lds + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
-    }
+// s_waitcnt vmcnt(VM) lgkmcnt(0), expcnt untouched (gfx9 encoding)
+template <int VM>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
 }
 
-template <int FM, int FN>
-__device__ __forceinline__ void read_frags(const char *sA, const char *sW, int r, int swz, int kk, int hi,
-                                           int wm0, int wn0, bf16x8 (&a)[FM], bf16x8 (&b)[FN]) {
+// Workgroup barrier with no memory fence: the caller has already waited for
+// the LDS traffic that must be complete (s_waitcnt), and the scheduling
+// barriers keep the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// CNT global -> LDS loads (16 bytes per lane, 1 KiB per wave and load) of one
+// operand into the 1 KiB blocks (q0 + j) * 4 + wave of `lds`.
+template <int CNT>
+__device__ __forceinline__ void load_blocks(__amdgpu_buffer_rsrc_t rsrc, char *lds, const uint32_t *off, int q0,
+                                            uint32_t kc2, int wave) {
+#pragma unroll
+    for (int j = 0; j < CNT; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_AS(lds + ((q0 + j) * 4 + wave) * 1024), 16,
+                                                 off[q0 + j] + kc2, 0, 0, 0);
+}
+
+// Fragments of MFMA substep kk of the stage in (sA, sW): ROWB-byte rows,
+// 16-byte chunk c of row r stored at chunk c ^ swz.
+template <int FM, int FN, int ROWB>
+__device__ __forceinline__ void read_frags(const char *sA, const char *sW, int r, int swz, int kk, int hi, int wm0,
+                                           int wn0, bf16x8 (&a)[FM], bf16x8 (&b)[FN]) {
     const int coff = ((2 * kk + hi) ^ swz) << 4;
 #pragma unroll
     for (int mi = 0; mi < FM; ++mi)
-        a[mi] = *reinterpret_cast<const bf16x8 *>(sA + (wm0 + mi * 32 + r) * 128 + coff);
+        a[mi] = *reinterpret_cast<const bf16x8 *>(sA + (wm0 + mi * 32 + r) * ROWB + coff);
 #pragma unroll
     for (int ni = 0; ni < FN; ++ni)
-        b[ni] = *reinterpret_cast<const bf16x8 *>(sW + (wn0 + ni * 32 + r) * 128 + coff);
+        b[ni] = *reinterpret_cast<const bf16x8 *>(sW + (wn0 + ni * 32 + r) * ROWB + coff);
 }
 
-// One K-stage (4 MFMA K-substeps of 16) on the LDS buffers sA/sW. Fragments
-// of substep kk+1 are read from LDS while the MFMAs of kk run (two register
-// sets), and the next stage's global->LDS loads (into dA/dW, when `load`) are
-// spread over the substeps; scheduling groups interleave the three streams.
-template <int BM, int BN, int FM, int FN>
-__device__ __forceinline__ void compute_stage(const char *sA, const char *sW, int lane, int wm0, int wn0,
-                                              f32x16 (&acc)[FN][FM], bool load, __amdgpu_buffer_rsrc_t rA,
-                                              __amdgpu_buffer_rsrc_t rW, char *dA, char *dW,
-                                              const uint32_t *offA, const uint32_t *offW, int cchunk, int k0n,
-                                              int K, int wave) {
-    constexpr int LA = BM / 32, LW = BN / 32;           // global loads per wave per stage
-    constexpr int LAK = LA / 4, LWK = LW / 4;           // ... per substep
-    const int r = lane & 31;
-    const int swz = (r >> 1) & 7;
-    const int hi = lane >> 5;
-    const int kc = k0n + cchunk * 8;
-    const bool kin = kc < K;
-    bf16x8 a[2][FM], b[2][FN];
-    read_frags<FM, FN>(sA, sW, r, swz, 0, hi, wm0, wn0, a[0], b[0]);
+// MFMAs [I0, I0 + CNT) of a substep (block i: acc[i / FM][i % FM]).
+template <int I0, int CNT, int FM, int FN>
+__device__ __forceinline__ void mfma_range(f32x16 (&acc)[FN][FM], const bf16x8 (&a)[FM], const bf16x8 (&b)[FN]) {
 #pragma unroll
-    for (int kk = 0; kk < kTileK / 16; ++kk) {
-        const int cur = kk & 1;
-        if (kk + 1 < kTileK / 16) read_frags<FM, FN>(sA, sW, r, swz, kk + 1, hi, wm0, wn0, a[cur ^ 1], b[cur ^ 1]);
-        if (load) {
+    for (int i = I0; i < I0 + CNT; ++i)
+        acc[i / FM][i % FM] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[i / FM], a[i % FM], acc[i / FM][i % FM], 0, 0, 0);
+}
+
+// Scheduling groups for the CNT MFMAs just emitted: one instruction of class
+// MASK (NX in all) after each MFMA, the rest after the last; then a barrier
+// that nothing is scheduled across.
+template <int CNT, int MASK, int NX>
+__device__ __forceinline__ void interleave() {
 #pragma unroll
-            for (int j = 0; j < LAK; ++j) {
-                const int q = kk * LAK + j;
-                const uint32_t off = (offA[q] == kOOB || !kin) ? kOOB : offA[q] + (uint32_t)kc * 2u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, LDS_AS(dA + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
-            }
-#pragma unroll
-            for (int j = 0; j < LWK; ++j) {
-                const int q = kk * LWK + j;
-                const uint32_t off = (offW[q] == kOOB || !kin) ? kOOB : offW[q] + (uint32_t)kc * 2u;
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rW, LDS_AS(dW + (q * 4 + wave) * 1024), 16, off, 0, 0, 0);
-            }
-        }
-#pragma unroll
-        for (int ni = 0; ni < FN; ++ni)
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi)
-                acc[ni][mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[cur][ni], a[cur][mi], acc[ni][mi], 0, 0, 0);
-        // per substep: FM*FN MFMAs, FM+FN LDS reads (next substep), LAK+LWK
-        // global loads; alternate MFMA with reads and loads
-        constexpr int NM = FM * FN, ND = FM + FN, NV = LAK + LWK;
-#pragma unroll
-        for (int i = 0; i < NM; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
-            if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
-        }
+    for (int i = 0; i < CNT - 1; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i < NX) __builtin_amdgcn_sched_group_barrier(MASK, 1, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (NX > CNT - 1) __builtin_amdgcn_sched_group_barrier(MASK, NX - (CNT - 1), 0);
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+constexpr int kDsRead = 0x100, kVmemRead = 0x020;
+
+// ---- 256 x 256 pipeline: four stages of K = 32
+constexpr int kBK4 = 32;
+
+// One stage on LDS buffers (cA, cW), whose substep-0 fragments are already
+// in (a0, b0). Substep 0: read substep 1's fragments, issue the A loads of
+// stage s + 3 into (dA, ...). Then wait until this wave's loads of stage
+// s + 1 have landed and join the barrier: after it, every wave's loads of
+// stage s + 1 are in LDS and every wave has finished reading the buffer the
+// stage s + 4 loads will overwrite. Substep 1: read stage s + 1's first
+// fragments from (nA, nW), issue the W loads of stage s + 3.
+template <int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void stage4(const char *cA, const char *cW, const char *nA, const char *nW, char *dA,
+                                       char *dW, f32x16 (&acc)[FN][FM], bf16x8 (&a0)[FM], bf16x8 (&b0)[FN],
+                                       bf16x8 (&a1)[FM], bf16x8 (&b1)[FN], __amdgpu_buffer_rsrc_t rA,
+                                       __amdgpu_buffer_rsrc_t rW, const uint32_t *offA, const uint32_t *offW,
+                                       uint32_t kc2, int r, int swz, int hi, int wm0, int wn0, int wave) {
+    constexpr int NM = FM * FN, H = NM / 2, ND = FM + FN;
+    constexpr int LA = BM / 64, LW = BN / 64;   // loads per wave per stage
+    read_frags<FM, FN, 64>(cA, cW, r, swz, 1, hi, wm0, wn0, a1, b1);
+    mfma_range<0, H, FM, FN>(acc, a0, b0);
+    interleave<H, kDsRead, ND>();
+    load_blocks<LA>(rA, dA, offA, 0, kc2, wave);
+    mfma_range<H, NM - H, FM, FN>(acc, a0, b0);
+    interleave<NM - H, kVmemRead, LA>();
+    // in flight after this wait: stage s + 2 (LA + LW) and the A half of s + 3
+    wait_vm_lgkm0<LA + LW + LA>();
+    lds_barrier();
+    read_frags<FM, FN, 64>(nA, nW, r, swz, 0, hi, wm0, wn0, a0, b0);
+    mfma_range<0, H, FM, FN>(acc, a1, b1);
+    interleave<H, kDsRead, ND>();
+    load_blocks<LW>(rW, dW, offW, 0, kc2, wave);
+    mfma_range<H, NM - H, FM, FN>(acc, a1, b1);
+    interleave<NM - H, kVmemRead, LW>();
+}
+
+// ---- 128 x 128 pipeline: two stages of K = 64
+constexpr int kBK2 = 64;
+
+// MFMA substep KK (of 4) of a stage on (sA, sW): read substep KK + 1's
+// fragments between the first half of the MFMAs; in substeps 0 and 1 issue
+// half of the next stage's loads into (dA, dW) between the second half.
+template <int KK, int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void substep2(const char *sA, const char *sW, char *dA, char *dW,
+                                         f32x16 (&acc)[FN][FM], bf16x8 (&a)[2][FM], bf16x8 (&b)[2][FN], bool load,
+                                         __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rW, const uint32_t *offA,
+                                         const uint32_t *offW, uint32_t kc2, int r, int swz, int hi, int wm0, int wn0,
+                                         int wave) {
+    constexpr int cur = KK & 1;
+    constexpr int NM = FM * FN, H = NM / 2, ND = FM + FN;
+    constexpr int LA = (KK < 2) ? BM / 64 : 0, LW = (KK < 2) ? BN / 64 : 0;   // half a stage's loads
+    if constexpr (KK + 1 < 4) read_frags<FM, FN, 128>(sA, sW, r, swz, KK + 1, hi, wm0, wn0, a[cur ^ 1], b[cur ^ 1]);
+    mfma_range<0, H, FM, FN>(acc, a[cur], b[cur]);
+    interleave<H, kDsRead, (KK + 1 < 4) ? ND : 0>();
+    if (load) {
+        load_blocks<LA>(rA, dA, offA, KK * LA, kc2, wave);
+        load_blocks<LW>(rW, dW, offW, KK * LW, kc2, wave);
+    }
+    mfma_range<H, NM - H, FM, FN>(acc, a[cur], b[cur]);
+    interleave<NM - H, kVmemRead, LA + LW>();
+}
+
+template <int BM, int BN, int FM, int FN>
+__device__ __forceinline__ void stage2(const char *sA, const char *sW, char *dA, char *dW, f32x16 (&acc)[FN][FM],
+                                       bool load, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rW,
+                                       const uint32_t *offA, const uint32_t *offW, uint32_t kc2, int r, int swz,
+                                       int hi, int wm0, int wn0, int wave) {
+    bf16x8 a[2][FM], b[2][FN];
+    read_frags<FM, FN, 128>(sA, sW, r, swz, 0, hi, wm0, wn0, a[0], b[0]);
+    substep2<0, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
+    substep2<1, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
+    substep2<2, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
+    substep2<3, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
 }
 
 // RS = false: optional main-loop gate (AllGather), plain store.
@@ -210,33 +311,56 @@ __global__ __launch_bounds__(kThreads, BM == 256 ? 1 : 2)
 void gemm_kernel(const GemmParams p) {
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
-    __shared__ __attribute__((aligned(1024))) char sA0[BM * 128];
-    __shared__ __attribute__((aligned(1024))) char sA1[BM * 128];
-    __shared__ __attribute__((aligned(1024))) char sW0[BN * 128];
-    __shared__ __attribute__((aligned(1024))) char sW1[BN * 128];
+    constexpr bool P4 = BM == 256;          // four stages of K = 32, else two of K = 64
+    constexpr int ROWB = P4 ? 64 : 128;     // LDS bytes per tile row and stage
+    constexpr int NOFF = P4 ? BM / 64 : BM / 32;   // loads per wave and stage (each operand)
+    static_assert(BM == BN && BM * ROWB == 16384, "both pipelines use 16 KiB per operand stage");
+    __shared__ __attribute__((aligned(1024))) char sA0[BM * ROWB];
+    __shared__ __attribute__((aligned(1024))) char sA1[BM * ROWB];
+    __shared__ __attribute__((aligned(1024))) char sA2[P4 ? BM * ROWB : 16];
+    __shared__ __attribute__((aligned(1024))) char sA3[P4 ? BM * ROWB : 16];
+    __shared__ __attribute__((aligned(1024))) char sW0[BN * ROWB];
+    __shared__ __attribute__((aligned(1024))) char sW1[BN * ROWB];
+    __shared__ __attribute__((aligned(1024))) char sW2[P4 ? BN * ROWB : 16];
+    __shared__ __attribute__((aligned(1024))) char sW3[P4 ? BN * ROWB : 16];
     __shared__ int s_pos;
     __shared__ int s_ok;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave >> 1) * WM;
     const int wn0 = (wave & 1) * WN;
     const int total = p.tiles_m * p.tiles_n;
-    const int KT2 = (((p.K + kTileK - 1) / kTileK) + 1) & ~1;
+    // stage counts rounded up so that the unrolled loops have no early exit
+    // (padding stages read only out-of-range columns, i.e. zeros)
+    const int KT4 = (((p.K + kBK4 - 1) / kBK4) + 3) & ~3;
+    const int KT2 = (((p.K + kBK2 - 1) / kBK2) + 1) & ~1;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
     const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, (int)p.w_bytes, 0x00020000);
 
-    // loader geometry: row of load q is 32 q + lrow0; logical chunk of the lane
-    const int lrow0 = 8 * wave + (lane >> 3);
-    const int cchunk = (lane & 7) ^ ((4 * wave + (lane >> 4)) & 7);
+    // loader geometry. Four stages: block q of this wave holds tile rows
+    // 64 q + 16 wave + (lane >> 2), physical chunk lane & 3. Two stages: rows
+    // 32 q + 8 wave + (lane >> 3), physical chunk lane & 7. A lane loads the
+    // logical chunk that the permutation puts at its physical chunk.
+    const int lrow0 = P4 ? 16 * wave + (lane >> 2) : 8 * wave + (lane >> 3);
+    const int cchunk = P4 ? (lane & 3) ^ ((lane >> 4) & 3) : (lane & 7) ^ ((4 * wave + (lane >> 4)) & 7);
+    const int r = lane & 31;                       // fragment row
+    const int hi = lane >> 5;                      // fragment K half
+    const int swz = P4 ? (r >> 2) & 3 : (r >> 1) & 7;
 
     uint64_t known = 0;   // partitions already acquired by this workgroup
     bool failed = false;
 
     if (tid == 0) {
+        if (p.spread_wait > 0 && claim_cu_slot(p) > 0) {
+            // bounded: a scheduling preference, never a dependency
+            const uint32_t t_end = rtc32() + 1000u;   // 10 us of the 100 MHz counter
+            while ((int)ld_dev(&p.ctrl[v]) < p.spread_wait && (int32_t)(rtc32() - t_end) < 0)
+                __builtin_amdgcn_s_sleep(2);
+        }
         const uint32_t c = __hip_atomic_fetch_add(&p.ctrl[v], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const int pos = ticket_position(p, v, c);
         if (pos == 0 && p.start_word)
@@ -259,6 +383,9 @@ void gemm_kernel(const GemmParams p) {
         const int n0 = tn * BN;
         const uint64_t touch = range_mask(p.rt_lo[rt], p.rt_hi[rt]);
         const uint64_t need = touch & ~p.resident_mask & ~known;
+        const bool traced = p.tile_trace && p.trace_base + (uint32_t)pos < p.trace_cap;
+        uint32_t t_tick = 0, t_gate = 0, t_loop = 0;
+        if (traced && tid == 0) t_tick = rtc32();
 
         if (!RS && p.gate == kGateMain && need) {
             if (tid == 0) s_ok = wait_flags(p, need);
@@ -266,6 +393,7 @@ void gemm_kernel(const GemmParams p) {
             if (!s_ok) failed = true;
             known |= need;
         }
+        if (traced && tid == 0) t_gate = rtc32();
 
         f32x16 acc[FN][FM];
 #pragma unroll
@@ -277,34 +405,63 @@ void gemm_kernel(const GemmParams p) {
 
         {   // a timed-out tile still runs (its loads stay in bounds); only its
             // stores are dropped
-            uint32_t offA[BM / 32], offW[BN / 32];
+            uint32_t offA[NOFF], offW[NOFF];
+            constexpr int RSTEP = BM / NOFF;       // tile rows between a wave's loads
 #pragma unroll
-            for (int q = 0; q < BM / 32; ++q) {
-                const int ia = m0 + 32 * q + lrow0;
+            for (int q = 0; q < NOFF; ++q) {
+                const int ia = m0 + RSTEP * q + lrow0;
                 offA[q] = ia < p.M ? (uint32_t)map_row(p, ia) * (uint32_t)p.lda * 2u : kOOB;
-            }
-#pragma unroll
-            for (int q = 0; q < BN / 32; ++q) {
-                const int iw = n0 + 32 * q + lrow0;
+                const int iw = n0 + RSTEP * q + lrow0;
                 offW[q] = iw < p.N ? (uint32_t)iw * (uint32_t)p.ldw * 2u : kOOB;
             }
-            load_stage<BM>(rA, sA0, offA, cchunk, 0, p.K, wave);
-            load_stage<BN>(rW, sW0, offW, cchunk, 0, p.K, wave);
-            // An even number of K-steps keeps the loop free of early exits (the
-            // accumulators then stay in place); a padding step reads only
-            // out-of-range columns, i.e. zeros.
-            for (int kt = 0; kt < KT2; kt += 2) {
+            auto kcol = [&](int st) -> uint32_t {   // byte offset of this lane's K chunk in stage st
+                const int kc = st * (P4 ? kBK4 : kBK2) + cchunk * 8;
+                return kc < p.K ? (uint32_t)kc * 2u : kOOB;
+            };
+            if constexpr (P4) {
+                constexpr int L = BM / 64;
+                // prologue: stages 0, 1, 2 in flight; stage 0 landed, its first fragments read
+                load_blocks<L>(rA, sA0, offA, 0, kcol(0), wave);
+                load_blocks<L>(rW, sW0, offW, 0, kcol(0), wave);
+                load_blocks<L>(rA, sA1, offA, 0, kcol(1), wave);
+                load_blocks<L>(rW, sW1, offW, 0, kcol(1), wave);
+                load_blocks<L>(rA, sA2, offA, 0, kcol(2), wave);
+                load_blocks<L>(rW, sW2, offW, 0, kcol(2), wave);
+                wait_vm_lgkm0<4 * L>();
+                lds_barrier();
+                bf16x8 a0[FM], b0[FN], a1[FM], b1[FN];
+                read_frags<FM, FN, 64>(sA0, sW0, r, swz, 0, hi, wm0, wn0, a0, b0);
+                for (int st = 0; st < KT4; st += 4) {
+                    stage4<BM, BN, FM, FN>(sA0, sW0, sA1, sW1, sA3, sW3, acc, a0, b0, a1, b1, rA, rW, offA, offW,
+                                           kcol(st + 3), r, swz, hi, wm0, wn0, wave);
+                    stage4<BM, BN, FM, FN>(sA1, sW1, sA2, sW2, sA0, sW0, acc, a0, b0, a1, b1, rA, rW, offA, offW,
+                                           kcol(st + 4), r, swz, hi, wm0, wn0, wave);
+                    stage4<BM, BN, FM, FN>(sA2, sW2, sA3, sW3, sA1, sW1, acc, a0, b0, a1, b1, rA, rW, offA, offW,
+                                           kcol(st + 5), r, swz, hi, wm0, wn0, wave);
+                    stage4<BM, BN, FM, FN>(sA3, sW3, sA0, sW0, sA2, sW2, acc, a0, b0, a1, b1, rA, rW, offA, offW,
+                                           kcol(st + 6), r, swz, hi, wm0, wn0, wave);
+                }
+                // the three stages loaded past the end (zeros) land before the
+                // buffers are reused
                 __builtin_amdgcn_s_waitcnt(0);
                 __syncthreads();
-                compute_stage<BM, BN, FM, FN>(sA0, sW0, lane, wm0, wn0, acc, true, rA, rW, sA1, sW1, offA, offW,
-                                              cchunk, (kt + 1) * kTileK, p.K, wave);
-                __builtin_amdgcn_s_waitcnt(0);
-                __syncthreads();
-                compute_stage<BM, BN, FM, FN>(sA1, sW1, lane, wm0, wn0, acc, kt + 2 < KT2, rA, rW, sA0, sW0, offA,
-                                              offW, cchunk, (kt + 2) * kTileK, p.K, wave);
+            } else {
+                load_blocks<NOFF>(rA, sA0, offA, 0, kcol(0), wave);
+                load_blocks<NOFF>(rW, sW0, offW, 0, kcol(0), wave);
+                for (int kt = 0; kt < KT2; kt += 2) {
+                    __builtin_amdgcn_s_waitcnt(0);
+                    __syncthreads();
+                    stage2<BM, BN, FM, FN>(sA0, sW0, sA1, sW1, acc, true, rA, rW, offA, offW, kcol(kt + 1), r, swz,
+                                           hi, wm0, wn0, wave);
+                    __builtin_amdgcn_s_waitcnt(0);
+                    __syncthreads();
+                    stage2<BM, BN, FM, FN>(sA1, sW1, sA0, sW0, acc, kt + 2 < KT2, rA, rW, offA, offW, kcol(kt + 2),
+                                           r, swz, hi, wm0, wn0, wave);
+                }
             }
         }
 
+        if (traced && tid == 0) t_loop = rtc32();
         // fetch the next ticket while the epilogue runs
         if (tid == 0) {
             const uint32_t c = __hip_atomic_fetch_add(&p.ctrl[v], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -318,36 +475,13 @@ void gemm_kernel(const GemmParams p) {
             known |= need;
         }
 
-        if (!RS) {
-            const int r = lane & 31;
-            const int hi = lane >> 5;
-            const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
-#pragma unroll
-            for (int mi = 0; mi < FM; ++mi) {
-                const int m = m0 + wm0 + mi * 32 + r;
-                if (m >= mlim) continue;
-                uint16_t *crow = p.C + (size_t)map_row(p, m) * p.ldc;
-#pragma unroll
-                for (int ni = 0; ni < FN; ++ni) {
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const int n = n0 + wn0 + ni * 32 + 8 * g + 4 * hi;
-                        if (n >= p.N) continue;
-                        uint2 o;
-                        o.x = pack_bf16x2(acc[ni][mi][4 * g + 0], acc[ni][mi][4 * g + 1]);
-                        o.y = pack_bf16x2(acc[ni][mi][4 * g + 2], acc[ni][mi][4 * g + 3]);
-                        *reinterpret_cast<uint2 *>(crow + n) = o;
-                    }
-                }
-            }
-        } else {
+        {
             // Each 32 x 32 fp32 block goes through a per-wave 4 KiB LDS patch
             // (rows of 128 bytes, 16-byte chunks XOR-permuted by row & 7) and
-            // comes back row-contiguous: 8 lanes per row add 128 contiguous
-            // bytes of the partial sum and store 64 contiguous bytes of C.
+            // comes back row-contiguous: 8 lanes per row read 128 contiguous
+            // bytes (adding as many bytes of the fp32 partial sum, if any) and
+            // store 64 contiguous bytes of C.
             char *patch = sA0 + wave * 4096;
-            const int r = lane & 31;
-            const int hi = lane >> 5;
             const int rr = lane >> 3;          // read-back row within 8
             const int rc = lane & 7;           // read-back chunk (4 floats)
             const int mlim = failed ? 0 : p.M;
@@ -372,7 +506,7 @@ void gemm_kernel(const GemmParams p) {
                         if (m < mlim && n < p.N) {
                             const int pm = map_row(p, m);
                             float v0 = x[0], v1 = x[1], v2 = x[2], v3 = x[3];
-                            if (p.P) {
+                            if (RS && p.P) {
                                 const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
                                 v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
                             }
@@ -402,6 +536,11 @@ void gemm_kernel(const GemmParams p) {
                     dm &= dm - 1;
                 }
             }
+        }
+        if (traced && tid == 0) {
+            uint4 *rec = reinterpret_cast<uint4 *>(p.tile_trace + (size_t)(p.trace_base + (uint32_t)pos) * kTraceWords);
+            rec[0] = make_uint4((uint32_t)pos, ((uint32_t)rt << 16) | (uint32_t)tn, hw_id(), xcc_id());
+            rec[1] = make_uint4(t_tick, t_gate, t_loop, rtc32());
         }
         pos = s_pos;
     }

@@ -33,6 +33,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
 #include <cstring>
 #include <deque>
 #include <memory>
@@ -73,6 +74,7 @@ static double now_s() {
 constexpr int kRoles = 4;            // in-fwd, in-bwd, out-fwd, out-bwd
 constexpr int kSignals = 256;        // completion signals per pacer
 constexpr size_t kDefaultSlice = 2u << 20;
+constexpr int kSchedFineQueues = 1, kSchedSpread = 2;
 // host_words layout (pinned, coherent host memory): start word, error word,
 // done flags (kernel -> copy side), arrival flags (copy side -> kernel)
 constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
@@ -81,7 +83,8 @@ constexpr int kHwWords = kHwFlags + kMaxFlags;
 constexpr int kCtrlDone = 64;
 constexpr int kCtrlMirror = kCtrlDone + kMaxFlags;
 constexpr int kCtrlLeader = kCtrlMirror + kMaxFlags;
-constexpr int kCtrlWords = kCtrlLeader + kMaxFlags;
+constexpr int kCtrlCuSlot = kCtrlLeader + kMaxFlags;
+constexpr int kCtrlWords = kCtrlCuSlot + kCuSlots;
 
 struct Item {
     void *dst;
@@ -115,6 +118,7 @@ struct Pacer {
     std::atomic<bool> stop{false};
     hsa_signal_t sig[kSignals];
     int sig_next = 0;
+    double lat_scale = 1.3;   // observed / modelled copy latency of paced items (biased late)
     void loop();
     void execute(Job &job);
     hsa_signal_t take_signal();
@@ -141,6 +145,11 @@ struct Ctx {
     static constexpr int kTimed = 512;
     hipEvent_t ev_begin[kTimed] = {}, ev_end[kTimed] = {};
     int timed_count = 0;             // launches recorded since the last read
+    uint32_t launch_seq = 0;         // tags the per-CU slot claims of a launch
+    int sched = kSchedFineQueues | kSchedSpread;
+    // optional per-tile trace records (device buffer of trace_cap records)
+    uint32_t *tile_trace = nullptr;
+    uint32_t trace_cap = 0, trace_used = 0;
     uint32_t engine_mask = 0;        // hardware engines allowed (0: all usable)
     // copy-side trace (COMPASS_TRACE=<file>): one line per event
     bool tracing = false;
@@ -255,10 +264,16 @@ static int ensure_init() {
         c.tracing = true;
         c.trace_path = tp;
     }
+    // Completion signals are polled by the pacer threads, never waited on:
+    // naming the GPU as their only consumer gives plain memory signals, with
+    // no interrupt raised per copy (COMPASS_SIGNALS=interrupt restores
+    // runtime-default signals).
+    const char *sm = std::getenv("COMPASS_SIGNALS");
+    const bool interrupt = sm && std::strcmp(sm, "interrupt") == 0;
     for (auto &p : c.pacer) {
         p.ctx = &c;
         for (auto &s : p.sig)
-            if (hsa_signal_create(0, 0, nullptr, &s) != HSA_STATUS_SUCCESS)
+            if (hsa_signal_create(0, interrupt ? 0 : 1, interrupt ? nullptr : &c.gpu, &s) != HSA_STATUS_SUCCESS)
                 return set_error(COMPASS_ERR_HIP, "hsa_signal_create failed");
     }
     // Usable SDMA engines: the runtime's availability mask only lists engines
@@ -372,10 +387,43 @@ static bool spin_until_epoch(volatile uint32_t *w, uint32_t epoch, double timeou
     return true;
 }
 
-// One job: issue every item's slices at their paced times (after the item's
-// gate opened), and publish an item's arrival flag, a release store of the
-// epoch into host memory, as soon as all of its slices have landed. Copies
-// carry no dependencies on one another; completion is observed here.
+// ---- paced links
+// Engine cost model for device-to-device SDMA copies measured on MI355X with
+// every engine busy: a copy of s bytes occupies its engine for about
+// kCopyFixed + s / kEngineBps. It sizes the engine groups and the lead time
+// of paced items; the observed latencies correct it as items land.
+constexpr double kCopyFixed = 10e-6;
+constexpr double kEngineBps = 38e9;
+
+// Engines per item for a paced job: the widest group (shortest item latency)
+// whose E / k groups still carry the link rate with 10 % headroom; if none
+// does, all E engines per item (the rate is then out of reach anyway, and
+// narrower groups would only add latency).
+static size_t group_width(double rate, size_t E, size_t item_bytes) {
+    for (size_t k = E; k >= 1; --k) {
+        if (E % k) continue;
+        const double lat = kCopyFixed + (double)item_bytes / ((double)k * kEngineBps);
+        if ((double)(E / k) * (double)item_bytes / lat >= 1.1 * rate) return k;
+    }
+    return E;
+}
+
+// One job.
+//
+// Paced (rate > 0): the emulated link carries one item at a time at `rate`,
+// so item i is due at link_free + bytes / rate, where link_free is when the
+// link finished the previous item (or when the item's gate opened, if
+// later). The item goes out whole on one group of k engines (groups taken in
+// turn), issued ahead of its due time by its predicted copy latency; its
+// arrival flag is published at the due time or when its copies have landed,
+// whichever is later. The kernel therefore never sees data before the link
+// would have delivered it.
+//
+// Unpaced (rate <= 0): slices go out round-robin over the engines as fast as
+// they are taken; an item's flag is published when its slices have landed.
+//
+// Flags are release stores of the epoch into host memory. Copies carry no
+// dependencies on one another; completion is observed here by polling.
 void Pacer::execute(Job &job) {
     Ctx &c = *ctx;
     if (job.items.empty() && job.final_flag < 0) return;
@@ -388,23 +436,60 @@ void Pacer::execute(Job &job) {
     struct Pend {
         int flag;
         size_t first, count;   // its signals in `issued`
+        double due;            // earliest publication time
+        double issued_at, model;
+        bool landed;
     };
     const size_t E = job.engines.size();
+    const bool paced = job.rate > 0;
+    size_t max_item = 0;
+    for (auto &it : job.items) max_item = std::max(max_item, it.bytes);
+    const size_t k = paced ? group_width(job.rate, E, max_item) : E;
+    const size_t groups = E / k;
     std::vector<hsa_signal_t> issued;
     std::vector<Pend> pend;
-    double t_next = now_s();
-    double last_progress = t_next;
+    double link_free = now_s();
+    double last_progress = link_free;
     size_t rr = 0, idx = 0, off = 0, item_first = 0;
     bool gate_ok = false;
+    double gate_time = 0;
+
+    auto issue = [&](const Item &it, size_t o, size_t len, size_t e) -> bool {
+        hsa_signal_t sg = take_signal();
+        const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
+            (char *)it.dst + o, it.dst_agent, (const char *)it.src + o, it.src_agent, len, 0, nullptr, sg,
+            (hsa_amd_sdma_engine_id_t)job.engines[e], true);
+        if (st != HSA_STATUS_SUCCESS) {
+            hsa_signal_store_relaxed(sg, 0);
+            c.async_err.store(COMPASS_ERR_HIP);
+            return false;
+        }
+        trace_event(role, job.epoch, "slice", __builtin_ctz(job.engines[e]), len);
+        issued.push_back(sg);
+        return true;
+    };
+
     for (;;) {
         bool progress = false;
+        const double now = now_s();
         for (size_t i = 0; i < pend.size();) {
-            bool landed = true;
-            for (size_t k = pend[i].first; k < pend[i].first + pend[i].count && landed; ++k)
-                landed = hsa_signal_load_scacquire(issued[k]) <= 0;
-            if (landed) {
-                __atomic_store_n(&c.hw[kHwFlags + pend[i].flag], job.epoch, __ATOMIC_RELEASE);
-                trace_event(role, job.epoch, "flag", pend[i].flag, 0);
+            Pend &pd = pend[i];
+            if (!pd.landed) {
+                bool landed = true;
+                for (size_t q = pd.first; q < pd.first + pd.count && landed; ++q)
+                    landed = hsa_signal_load_scacquire(issued[q]) <= 0;
+                if (landed) {
+                    pd.landed = true;
+                    if (paced && pd.model > 0) {
+                        // latency correction, biased late: an early item only waits for its due time
+                        const double ratio = (now - pd.issued_at) / pd.model;
+                        lat_scale = 0.7 * lat_scale + 0.3 * std::min(4.0, std::max(0.5, 1.15 * ratio));
+                    }
+                }
+            }
+            if (pd.landed && now >= pd.due) {
+                __atomic_store_n(&c.hw[kHwFlags + pd.flag], job.epoch, __ATOMIC_RELEASE);
+                trace_event(role, job.epoch, "flag", pd.flag, 0);
                 pend.erase(pend.begin() + (long)i);
                 progress = true;
             } else {
@@ -416,35 +501,46 @@ void Pacer::execute(Job &job) {
             if (it.gate >= 0 && !gate_ok &&
                 (int32_t)(__atomic_load_n(&c.hw[kHwDone + it.gate], __ATOMIC_ACQUIRE) - job.epoch) >= 0) {
                 gate_ok = true;
-                t_next = std::max(t_next, now_s());
+                gate_time = now_s();
                 trace_event(role, job.epoch, "gate_open", it.gate, 0);
             }
-            if ((it.gate < 0 || gate_ok) && (job.rate <= 0 || now_s() >= t_next)) {
-                if (off == 0) item_first = issued.size();
-                if (off < it.bytes) {
-                    const size_t len = std::min(job.slice, it.bytes - off);
-                    if (job.rate > 0) t_next += (double)len / job.rate;
-                    const size_t e = rr++ % E;
-                    hsa_signal_t sg = take_signal();
-                    const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
-                        (char *)it.dst + off, it.dst_agent, (const char *)it.src + off, it.src_agent, len, 0,
-                        nullptr, sg, (hsa_amd_sdma_engine_id_t)job.engines[e], true);
-                    if (st != HSA_STATUS_SUCCESS) {
-                        hsa_signal_store_relaxed(sg, 0);
-                        c.async_err.store(COMPASS_ERR_HIP);
-                        return;
+            if (it.gate < 0 || gate_ok) {
+                if (paced) {
+                    const double start = std::max(link_free, it.gate >= 0 ? gate_time : 0.0);
+                    const double due = start + (double)it.bytes / job.rate;
+                    const double model = kCopyFixed + (double)it.bytes / ((double)k * kEngineBps);
+                    if (now_s() >= due - model * lat_scale) {
+                        const size_t first = issued.size();
+                        const size_t g0 = (idx % groups) * k;
+                        size_t per = (it.bytes + k - 1) / k;
+                        per = std::min((per + 255) & ~(size_t)255, job.slice);
+                        size_t o = 0, j = 0;
+                        while (o < it.bytes) {
+                            const size_t len = std::min(per, it.bytes - o);
+                            if (!issue(it, o, len, g0 + (j++ % k))) return;
+                            o += len;
+                        }
+                        if (it.flag >= 0) pend.push_back({it.flag, first, issued.size() - first, due, now_s(), model, false});
+                        link_free = due;
+                        ++idx;
+                        gate_ok = false;
+                        progress = true;
                     }
-                    trace_event(role, job.epoch, "slice", __builtin_ctz(job.engines[e]), len);
-                    issued.push_back(sg);
-                    off += len;
+                } else {
+                    if (off == 0) item_first = issued.size();
+                    if (off < it.bytes) {
+                        const size_t len = std::min(job.slice, it.bytes - off);
+                        if (!issue(it, off, len, rr++ % E)) return;
+                        off += len;
+                    }
+                    if (off >= it.bytes) {
+                        if (it.flag >= 0) pend.push_back({it.flag, item_first, issued.size() - item_first, 0.0, 0.0, 0.0, false});
+                        ++idx;
+                        off = 0;
+                        gate_ok = false;
+                    }
+                    progress = true;
                 }
-                if (off >= it.bytes) {
-                    if (it.flag >= 0) pend.push_back({it.flag, item_first, issued.size() - item_first});
-                    ++idx;
-                    off = 0;
-                    gate_ok = false;
-                }
-                progress = true;
             }
         } else if (pend.empty()) {
             break;
@@ -452,7 +548,10 @@ void Pacer::execute(Job &job) {
         if (progress) {
             last_progress = now_s();
         } else {
-            if (now_s() - last_progress > c.host_timeout) {
+            // waiting for a due time (paced) is not a stall
+            double horizon = last_progress;
+            if (paced) horizon = std::max(horizon, link_free + (double)max_item / job.rate);
+            if (now_s() - horizon > c.host_timeout) {
                 c.async_err.store(COMPASS_ERR_TIMEOUT);
                 return;
             }
@@ -555,9 +654,9 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     if (p->M % P) return set_error(COMPASS_ERR_INVALID, "M must be divisible by %d", P);
     if (p->K % 8 || p->N % 8) return set_error(COMPASS_ERR_INVALID, "K and N must be multiples of 8");
     if ((p->M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
-    if ((double)p->M * p->K * 2 >= 2147483648.0 || (double)p->N * p->K * 2 >= 2147483648.0 ||
+    if ((double)p->M * p->K * 2 > 1073741824.0 || (double)p->N * p->K * 2 > 1073741824.0 ||
         (double)p->M * p->N * 4 >= 2147483648.0)
-        return set_error(COMPASS_ERR_UNSUPPORTED, "operand larger than 2 GiB");
+        return set_error(COMPASS_ERR_UNSUPPORTED, "A or W above 1 GiB, or M x N fp32 above 2 GiB");
     if (!p->W || !p->C) return set_error(COMPASS_ERR_INVALID, "W and C are required");
     if (p->pattern == COMPASS_AG_GEMM) {
         if (!p->shard_src || !p->gathered) return set_error(COMPASS_ERR_INVALID, "shard_src and gathered are required");
@@ -573,6 +672,9 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     }
     if (l->slice_bytes != 0 && l->slice_bytes < 4096) return set_error(COMPASS_ERR_INVALID, "slice_bytes below 4 KiB");
     if (l->engines_per_ring < 0) return set_error(COMPASS_ERR_INVALID, "engines_per_ring < 0");
+    for (double r : {l->fwd_Bps, l->bwd_Bps})
+        if (!std::isfinite(r) || (r > 0 && r < 1e8))
+            return set_error(COMPASS_ERR_INVALID, "link rates must be <= 0 (unpaced) or at least 1e8 bytes/s");
     g->P = P;
     g->rows = p->M / p->n;
     g->prow = p->M / P;
@@ -590,6 +692,7 @@ static void init_params(GemmParams &g, uint32_t epoch) {
     g.leader = c.ctrl + kCtrlLeader;
     g.ctrl = c.ctrl;
     g.done_cnt = c.ctrl + kCtrlDone;
+    g.cu_slots = c.ctrl + kCtrlCuSlot;
     g.err_word = &c.hw[kHwErr];
     g.spin_limit = c.spin_limit;
     g.epoch = epoch;
@@ -656,6 +759,13 @@ static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M
     }
     std::stable_sort(key.begin(), key.end());
     for (int i = 0; i < g.tiles_m; ++i) g.rt_order[i] = (uint16_t)key[i].second;
+    // Tiles of one arriving partition are consecutive in the ready order:
+    // short super-blocks deal them out over all XCD queues, and the second
+    // workgroup of each CU waits for the first tickets to go one per CU.
+    if (g_ctx.sched & kSchedFineQueues) g.q_size = std::max(1, g.group_m);
+    if ((g_ctx.sched & kSchedSpread) && g.nq == kMaxQueues && g.grid == g_ctx.num_cu * tile_wg_per_cu(cfg) &&
+        tile_wg_per_cu(cfg) > 1)
+        g.spread_wait = g_ctx.num_cu / kMaxQueues;
 }
 
 static inline uint64_t touched(const GemmParams &g, int t) {
@@ -819,8 +929,17 @@ static int stage_resident_partials(const compass_problem *p, const Geometry &geo
     return COMPASS_OK;
 }
 
-static int launch(const GemmParams &g, int cfg, bool rs, hipStream_t s) {
+static int launch(const GemmParams &g0, int cfg, bool rs, hipStream_t s) {
     Ctx &c = g_ctx;
+    GemmParams g = g0;
+    if (++c.launch_seq == 0) c.launch_seq = 1;
+    g.launch_seq = c.launch_seq;
+    if (c.tile_trace) {
+        g.tile_trace = c.tile_trace;
+        g.trace_base = c.trace_used;
+        g.trace_cap = c.trace_cap;
+        c.trace_used = std::min<uint64_t>(c.trace_cap, (uint64_t)c.trace_used + (uint64_t)g0.tiles_m * g0.tiles_n);
+    }
     const bool timed = c.timing && c.timed_count < Ctx::kTimed;
     if (timed) hipEventRecord(c.ev_begin[c.timed_count], s);
     const hipError_t e = launch_gemm(g, cfg, rs, s);
@@ -842,6 +961,19 @@ int op_kernel_times(double *us, int cap) {
         us[i] = (double)ms * 1e3;
     }
     c.timed_count = 0;
+    return n;
+}
+
+int op_tile_trace(uint32_t *out, int cap) {
+    Ctx &c = g_ctx;
+    if (!c.ready || !c.tile_trace) return set_error(COMPASS_ERR_INVALID, "tile trace is not enabled");
+    if (cap < 0 || (cap > 0 && !out)) return set_error(COMPASS_ERR_INVALID, "bad output buffer");
+    const int n = (int)std::min<uint32_t>((uint32_t)cap, c.trace_used);
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess && n > 0)
+        e = hipMemcpy(out, c.tile_trace, (size_t)n * kTraceWords * sizeof(uint32_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "tile trace read");
+    c.trace_used = 0;
     return n;
 }
 
@@ -999,8 +1131,8 @@ int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const fl
     if (M < 1 || N < 1 || K < 1 || K % 8 || N % 8) return set_error(COMPASS_ERR_INVALID, "need positive M, N, K with K, N multiples of 8");
     if (!A || !W || !C) return set_error(COMPASS_ERR_INVALID, "A, W and C are required");
     if ((M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
-    if ((double)M * K * 2 >= 2147483648.0 || (double)N * K * 2 >= 2147483648.0 || (double)M * N * 4 >= 2147483648.0)
-        return set_error(COMPASS_ERR_UNSUPPORTED, "operand larger than 2 GiB");
+    if ((double)M * K * 2 > 1073741824.0 || (double)N * K * 2 > 1073741824.0 || (double)M * N * 4 >= 2147483648.0)
+        return set_error(COMPASS_ERR_UNSUPPORTED, "A or W above 1 GiB, or M x N fp32 above 2 GiB");
     int rc = begin();
     if (rc != COMPASS_OK) return rc;
     GemmParams g;
@@ -1123,6 +1255,31 @@ int op_set_option(int key, long long v) {
         c.timed_count = 0;
         return COMPASS_OK;
     }
+    case COMPASS_OPT_TILE_TRACE: {
+        if (v < 0 || v > (1 << 20)) return set_error(COMPASS_ERR_INVALID, "tile trace capacity out of range");
+        const int rc = ensure_init();
+        if (rc != COMPASS_OK) return rc;
+        if (c.tile_trace) {
+            hipError_t e = hipDeviceSynchronize();
+            if (e == hipSuccess) e = hipFree(c.tile_trace);
+            c.tile_trace = nullptr;
+            c.trace_cap = c.trace_used = 0;
+            if (e != hipSuccess) return hip_fail(e, "tile trace free");
+        }
+        if (v > 0) {
+            const hipError_t e = hipMalloc((void **)&c.tile_trace, (size_t)v * kTraceWords * sizeof(uint32_t));
+            if (e != hipSuccess) {
+                c.tile_trace = nullptr;
+                return hip_fail(e, "tile trace allocation");
+            }
+            c.trace_cap = (uint32_t)v;
+        }
+        return COMPASS_OK;
+    }
+    case COMPASS_OPT_SCHED:
+        if (v < 0 || v > 3) return set_error(COMPASS_ERR_INVALID, "schedule option must be in [0, 3]");
+        c.sched = (int)v;
+        return COMPASS_OK;
     case COMPASS_OPT_DROP_FLAG:
         if (v < -1 || v >= 2 * kMaxRanks) return set_error(COMPASS_ERR_INVALID, "drop flag out of range");
         c.drop_flag = (int)v;
