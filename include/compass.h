@@ -215,9 +215,13 @@ int compass_sync(void);
 #define COMPASS_OPT_TILE_TRACE   8  /* > 0: record one timing record per output tile of
                                        every GEMM launch, up to this many records
                                        (a device buffer of value * 32 bytes); 0 = off */
-#define COMPASS_OPT_SCHED        9  /* tile dealing of gated operators, bit mask (default 3):
-                                       1 = super-blocks of one row-tile group per XCD
-                                       queue, 2 = first tickets spread one per CU */
+#define COMPASS_OPT_SCHED        9  /* work dealing, bit mask (default 7): 1 = gated
+                                       operators deal one row-tile group per XCD queue,
+                                       2 = their first tickets go one per CU, 4 = GEMMs
+                                       that do not gate (plain, InterDecom, unfused) with
+                                       fewer tiles than half the workgroup slots split K
+                                       (fp32 partial tiles in a library workspace of
+                                       CUs x 256 KiB, summed in slice order) */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

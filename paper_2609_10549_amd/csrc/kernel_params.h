@@ -14,6 +14,8 @@ constexpr int kMaxQueues = 8;        // ticket queues (one per XCD)
 constexpr int kCtrlExit = kMaxQueues;       // ctrl word: exit counter
 constexpr int kTraceWords = 8;       // words per tile-trace record
 constexpr int kCuSlots = 8 * 256;    // ctrl words: per (XCC, SE/SH/CU id) slot claims
+constexpr int kMaxSplitTiles = 512;  // tiles of a split-K launch (one counter each)
+constexpr int kMaxSplit = 16;        // K slices per tile
 
 // Tile configurations of the GEMM kernel.
 enum TileCfg : int {
@@ -56,6 +58,14 @@ struct GemmParams {
     int spread_wait;
     uint32_t launch_seq;
     uint32_t *cu_slots;
+    // split K: tile position t, slice j = work position t * ksplit + j, K
+    // range [j kslice, (j + 1) kslice). Every slice stores its fp32 partial
+    // tile at split_ws[(t * ksplit + j) * BM * BN]; the slice that counts
+    // split_cnt[t] up to ksplit sums the partials in slice order and runs the
+    // epilogue. ksplit == 1: no split (kslice = K).
+    int ksplit, kslice;
+    uint32_t *split_cnt;
+    float *split_ws;
     // gating: flag index of partition p is flag_base + p. Arrival flags live
     // in pinned host memory (written by the copy-side threads); the first
     // workgroup that needs a partition in an epoch (`leader`) polls it and

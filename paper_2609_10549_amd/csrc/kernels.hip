@@ -76,36 +76,40 @@ __device__ __forceinline__ bool poll_epoch(const uint32_t *w, bool host, uint32_
     return true;
 }
 
-// Thread-0 wait for every partition in `mask`. Per partition and epoch one
-// workgroup (the first to claim `leader`) polls the host-memory arrival flag
-// and forwards it to `mirror` in device memory; every other workgroup polls
-// the mirror. A system-scope acquire follows, so that the rows the copy
-// engines wrote are read from memory, not from stale cache lines.
-__device__ bool wait_flags(const GemmParams &p, uint64_t mask) {
-    while (mask) {
-        const int f = p.flag_base + __builtin_ctzll(mask);
-        mask &= mask - 1;
-        if ((int32_t)(ld_dev(&p.mirror[f]) - p.epoch) >= 0) continue;
-        uint32_t cur = ld_dev(&p.leader[f]);
-        bool lead = false;
-        while ((int32_t)(cur - p.epoch) < 0) {
-            uint32_t expect = cur;
-            if (__hip_atomic_compare_exchange_strong(&p.leader[f], &expect, p.epoch, __ATOMIC_RELAXED,
-                                                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-                lead = true;
-                break;
+// Wait of wave 0 for every partition in `mask` (bit q: partition q, at most
+// 64): lane q handles partition q, so the flags are polled in parallel. Per
+// partition and epoch one workgroup (the first to claim `leader`) polls the
+// host-memory arrival flag and forwards it to `mirror` in device memory;
+// every other workgroup polls the mirror. A system-scope acquire follows, so
+// that the rows the copy engines wrote are read from memory, not from stale
+// cache lines. True when every partition arrived (false: bound or error).
+__device__ bool wait_flags(const GemmParams &p, uint64_t mask, int lane) {
+    bool ok = true;
+    if ((mask >> lane) & 1ull) {
+        const int f = p.flag_base + lane;
+        if ((int32_t)(ld_dev(&p.mirror[f]) - p.epoch) < 0) {
+            uint32_t cur = ld_dev(&p.leader[f]);
+            bool lead = false;
+            while ((int32_t)(cur - p.epoch) < 0) {
+                uint32_t expect = cur;
+                if (__hip_atomic_compare_exchange_strong(&p.leader[f], &expect, p.epoch, __ATOMIC_RELAXED,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+                    lead = true;
+                    break;
+                }
+                cur = expect;
             }
-            cur = expect;
-        }
-        if (lead) {
-            if (!poll_epoch(&p.flags[f], true, p.epoch, p.spin_limit, p.err_word, 16)) return false;
-            __hip_atomic_store(&p.mirror[f], p.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            if (!poll_epoch(&p.mirror[f], false, p.epoch, p.spin_limit, p.err_word, 4)) return false;
+            if (lead) {
+                ok = poll_epoch(&p.flags[f], true, p.epoch, p.spin_limit, p.err_word, 16);
+                if (ok) __hip_atomic_store(&p.mirror[f], p.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                ok = poll_epoch(&p.mirror[f], false, p.epoch, p.spin_limit, p.err_word, 4);
+            }
         }
     }
+    const bool all_ok = __ballot(!ok) == 0ull;
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-    return true;
+    return all_ok;
 }
 
 __device__ __forceinline__ uint32_t rtc32() { return (uint32_t)__builtin_amdgcn_s_memrealtime(); }
@@ -325,17 +329,14 @@ void gemm_kernel(const GemmParams p) {
     __shared__ __attribute__((aligned(1024))) char sW3[P4 ? BN * ROWB : 16];
     __shared__ int s_pos;
     __shared__ int s_ok;
+    __shared__ int s_last;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave >> 1) * WM;
     const int wn0 = (wave & 1) * WN;
-    const int total = p.tiles_m * p.tiles_n;
-    // stage counts rounded up so that the unrolled loops have no early exit
-    // (padding stages read only out-of-range columns, i.e. zeros)
-    const int KT4 = (((p.K + kBK4 - 1) / kBK4) + 3) & ~3;
-    const int KT2 = (((p.K + kBK2 - 1) / kBK2) + 1) & ~1;
+    const int total = p.tiles_m * p.tiles_n * p.ksplit;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
     const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
@@ -371,10 +372,15 @@ void gemm_kernel(const GemmParams p) {
     int pos = s_pos;
 
     while (pos < total) {
-        // position -> (row-tile ordinal, column tile): group_m rows at a time
+        // work position -> (tile position, K slice)
+        const int tpos = p.ksplit > 1 ? pos / p.ksplit : pos;
+        const int slice = pos - tpos * p.ksplit;
+        const int kb = slice * p.kslice;
+        const int ke = min(p.K, kb + p.kslice);
+        // tile position -> (row-tile ordinal, column tile): group_m rows at a time
         const int gsz = p.group_m * p.tiles_n;
-        const int grp = pos / gsz;
-        const int rin = pos - grp * gsz;
+        const int grp = tpos / gsz;
+        const int rin = tpos - grp * gsz;
         const int rows_here = min(p.group_m, p.tiles_m - grp * p.group_m);
         const int ti = grp * p.group_m + rin % rows_here;
         const int tn = rin / rows_here;
@@ -388,7 +394,10 @@ void gemm_kernel(const GemmParams p) {
         if (traced && tid == 0) t_tick = rtc32();
 
         if (!RS && p.gate == kGateMain && need) {
-            if (tid == 0) s_ok = wait_flags(p, need);
+            if (wave == 0) {
+                const bool ok = wait_flags(p, need, lane);
+                if (lane == 0) s_ok = ok;
+            }
             __syncthreads();
             if (!s_ok) failed = true;
             known |= need;
@@ -415,9 +424,13 @@ void gemm_kernel(const GemmParams p) {
                 offW[q] = iw < p.N ? (uint32_t)iw * (uint32_t)p.ldw * 2u : kOOB;
             }
             auto kcol = [&](int st) -> uint32_t {   // byte offset of this lane's K chunk in stage st
-                const int kc = st * (P4 ? kBK4 : kBK2) + cchunk * 8;
-                return kc < p.K ? (uint32_t)kc * 2u : kOOB;
+                const int kc = kb + st * (P4 ? kBK4 : kBK2) + cchunk * 8;
+                return kc < ke ? (uint32_t)kc * 2u : kOOB;
             };
+            // stage counts rounded up so that the unrolled loops have no early
+            // exit (padding stages read only out-of-range columns, i.e. zeros)
+            const int KT4 = (((ke - kb + kBK4 - 1) / kBK4) + 3) & ~3;
+            const int KT2 = (((ke - kb + kBK2 - 1) / kBK2) + 1) & ~1;
             if constexpr (P4) {
                 constexpr int L = BM / 64;
                 // prologue: stages 0, 1, 2 in flight; stage 0 landed, its first fragments read
@@ -468,23 +481,14 @@ void gemm_kernel(const GemmParams p) {
             s_pos = ticket_position(p, v, c);
         }
 
-        if (RS && p.gate == kGateEpilogue && need) {
-            if (tid == 0) s_ok = failed ? 0 : wait_flags(p, need);
-            __syncthreads();
-            if (!s_ok) failed = true;
-            known |= need;
-        }
-
-        {
-            // Each 32 x 32 fp32 block goes through a per-wave 4 KiB LDS patch
-            // (rows of 128 bytes, 16-byte chunks XOR-permuted by row & 7) and
-            // comes back row-contiguous: 8 lanes per row read 128 contiguous
-            // bytes (adding as many bytes of the fp32 partial sum, if any) and
-            // store 64 contiguous bytes of C.
-            char *patch = sA0 + wave * 4096;
+        // Each 32 x 32 fp32 block of the accumulators goes through a per-wave
+        // 4 KiB LDS patch (rows of 128 bytes, 16-byte chunks XOR-permuted by
+        // row & 7) and comes back row-contiguous: 8 lanes per row hold 128
+        // contiguous bytes. `emit(tile row, tile column, 4 values)`.
+        char *patch = sA0 + wave * 4096;
+        auto through_patch = [&](auto &&emit) {
             const int rr = lane >> 3;          // read-back row within 8
             const int rc = lane & 7;           // read-back chunk (4 floats)
-            const int mlim = failed ? 0 : p.M;
 #pragma unroll
             for (int mi = 0; mi < FM; ++mi) {
 #pragma unroll
@@ -501,28 +505,93 @@ void gemm_kernel(const GemmParams p) {
                     for (int it = 0; it < 4; ++it) {
                         const int row = rr + 8 * it;
                         const f32x4 x = *reinterpret_cast<const f32x4 *>(patch + row * 128 + ((rc ^ (row & 7)) << 4));
-                        const int m = m0 + wm0 + mi * 32 + row;
-                        const int n = n0 + wn0 + ni * 32 + 4 * rc;
-                        if (m < mlim && n < p.N) {
-                            const int pm = map_row(p, m);
-                            float v0 = x[0], v1 = x[1], v2 = x[2], v3 = x[3];
-                            if (RS && p.P) {
-                                const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
-                                v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
-                            }
-                            uint2 o;
-                            o.x = pack_bf16x2(v0, v1);
-                            o.y = pack_bf16x2(v2, v3);
-                            *reinterpret_cast<uint2 *>(p.C + (size_t)pm * p.ldc + n) = o;
-                        }
+                        emit(wm0 + mi * 32 + row, wn0 + ni * 32 + 4 * rc, x);
                     }
                     __builtin_amdgcn_s_waitcnt(0xC07F);   // patch read before reuse
                 }
             }
+        };
+        const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
+        // bf16 store of 4 values at tile (row, col), after adding the fp32
+        // partial sum (ReduceScatter): 64 contiguous bytes of C per row
+        auto store4 = [&](int row, int col, float v0, float v1, float v2, float v3) {
+            const int m = m0 + row, n = n0 + col;
+            if (m < mlim && n < p.N) {
+                const int pm = map_row(p, m);
+                if (RS && p.P) {
+                    const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
+                    v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
+                }
+                uint2 o;
+                o.x = pack_bf16x2(v0, v1);
+                o.y = pack_bf16x2(v2, v3);
+                *reinterpret_cast<uint2 *>(p.C + (size_t)pm * p.ldc + n) = o;
+            }
+        };
+
+        // split K: every slice stores its partial tile (fp32, row-major);
+        // the slice that completes the tile's count sums all of them in
+        // slice order, so the result does not depend on which one was last
+        bool finish = true;
+        if (p.ksplit > 1) {
+            float *ws = p.split_ws + (size_t)(tpos * p.ksplit + slice) * (BM * BN);
+            through_patch([&](int row, int col, f32x4 x) {
+                *reinterpret_cast<f32x4 *>(ws + row * BN + col) = x;
+            });
+            // The workspace is uncached device memory: a store acknowledged
+            // to the wave is in memory, visible to every XCD, and loads read
+            // memory. So ordering needs no cache maintenance: each wave waits
+            // for its stores, the barrier joins the waves, then the count.
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (tid == 0) {
+                const uint32_t old = __hip_atomic_fetch_add(&p.split_cnt[tpos], 1u, __ATOMIC_RELAXED,
+                                                            __HIP_MEMORY_SCOPE_AGENT);
+                const bool last = old + 1u == (uint32_t)p.ksplit;
+                if (last) __hip_atomic_store(&p.split_cnt[tpos], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                s_last = last;
+            }
+            __syncthreads();   // the partial loads below are issued after the count
+            finish = s_last != 0;
+        }
+
+        if (RS && finish && p.gate == kGateEpilogue && need) {
+            if (wave == 0) {
+                const bool ok = !failed && wait_flags(p, need, lane);
+                if (lane == 0) s_ok = ok;
+            }
+            __syncthreads();
+            if (!s_ok) failed = true;
+            known |= need;
+        }
+
+        if (finish) {
+            if (p.ksplit > 1) {
+                const float *ws0 = p.split_ws + (size_t)tpos * p.ksplit * (BM * BN);
+                for (int e = tid; e < BM * BN / 4; e += kThreads) {
+                    const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
+                    // every slice's load in flight at once, then the sum in slice order
+                    f32x4 part[kMaxSplit];
+#pragma unroll
+                    for (int jj = 0; jj < kMaxSplit; ++jj)
+                        if (jj < p.ksplit)
+                            part[jj] = *reinterpret_cast<const f32x4 *>(ws0 + (size_t)jj * (BM * BN) + row * BN + col);
+                    f32x4 sum = part[0];
+#pragma unroll
+                    for (int jj = 1; jj < kMaxSplit; ++jj)
+                        if (jj < p.ksplit) {
+                            sum[0] += part[jj][0]; sum[1] += part[jj][1];
+                            sum[2] += part[jj][2]; sum[3] += part[jj][3];
+                        }
+                    store4(row, col, sum[0], sum[1], sum[2], sum[3]);
+                }
+            } else {
+                through_patch([&](int row, int col, f32x4 x) { store4(row, col, x[0], x[1], x[2], x[3]); });
+            }
         }
 
         __syncthreads();   // stores issued and complete; LDS free for the next tile
-        if (RS && p.done_host && !failed && tid == 0) {
+        if (RS && finish && p.done_host && !failed && tid == 0) {
             uint64_t dm = touch & p.send_mask;
             if (dm) {
                 __threadfence_system();   // tile data written back before counting

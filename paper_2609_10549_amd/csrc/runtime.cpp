@@ -74,7 +74,10 @@ static double now_s() {
 constexpr int kRoles = 4;            // in-fwd, in-bwd, out-fwd, out-bwd
 constexpr int kSignals = 256;        // completion signals per pacer
 constexpr size_t kDefaultSlice = 2u << 20;
-constexpr int kSchedFineQueues = 1, kSchedSpread = 2;
+constexpr int kSchedFineQueues = 1, kSchedSpread = 2, kSchedSplitK = 4;
+// split-K workspace: one fp32 partial tile per workgroup slot (the largest
+// of 256 x 256 on one workgroup per CU and 128 x 128 on two)
+constexpr int kMinSliceK = 512;      // K depth of a slice at least
 // host_words layout (pinned, coherent host memory): start word, error word,
 // done flags (kernel -> copy side), arrival flags (copy side -> kernel)
 constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
@@ -84,7 +87,8 @@ constexpr int kCtrlDone = 64;
 constexpr int kCtrlMirror = kCtrlDone + kMaxFlags;
 constexpr int kCtrlLeader = kCtrlMirror + kMaxFlags;
 constexpr int kCtrlCuSlot = kCtrlLeader + kMaxFlags;
-constexpr int kCtrlWords = kCtrlCuSlot + kCuSlots;
+constexpr int kCtrlSplit = kCtrlCuSlot + kCuSlots;
+constexpr int kCtrlWords = kCtrlSplit + kMaxSplitTiles;
 
 struct Item {
     void *dst;
@@ -146,7 +150,9 @@ struct Ctx {
     hipEvent_t ev_begin[kTimed] = {}, ev_end[kTimed] = {};
     int timed_count = 0;             // launches recorded since the last read
     uint32_t launch_seq = 0;         // tags the per-CU slot claims of a launch
-    int sched = kSchedFineQueues | kSchedSpread;
+    int sched = kSchedFineQueues | kSchedSpread | kSchedSplitK;
+    float *split_ws = nullptr;       // device, split_ws_bytes
+    size_t split_ws_bytes = 0;
     // optional per-tile trace records (device buffer of trace_cap records)
     uint32_t *tile_trace = nullptr;
     uint32_t trace_cap = 0, trace_used = 0;
@@ -258,6 +264,15 @@ static int ensure_init() {
         return hip_fail(e, "host word allocation");
     std::memset(c.hw, 0, kHwWords * sizeof(uint32_t));
     if ((e = hipMemset(c.ctrl, 0, kCtrlWords * sizeof(uint32_t))) != hipSuccess) return hip_fail(e, "control clear");
+    {
+        // Uncached, so that partial tiles written on one XCD are read on
+        // another without cache maintenance. Held until the process ends
+        // (uncached memory is never freed once a kernel has read it).
+        const size_t ws = (size_t)c.num_cu * std::max(256 * 256, 2 * 128 * 128) * sizeof(float);
+        if ((e = hipExtMallocWithFlags((void **)&c.split_ws, ws, hipDeviceMallocUncached)) != hipSuccess)
+            return hip_fail(e, "split-K workspace");
+        c.split_ws_bytes = ws;
+    }
     if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "init sync");
     for (int r = 0; r < kRoles; ++r) c.pacer[r].role = r;
     if (const char *tp = std::getenv("COMPASS_TRACE")) {
@@ -693,18 +708,24 @@ static void init_params(GemmParams &g, uint32_t epoch) {
     g.ctrl = c.ctrl;
     g.done_cnt = c.ctrl + kCtrlDone;
     g.cu_slots = c.ctrl + kCtrlCuSlot;
+    g.split_cnt = c.ctrl + kCtrlSplit;
+    g.split_ws = c.split_ws;
+    g.ksplit = 1;
     g.err_word = &c.hw[kHwErr];
     g.spin_limit = c.spin_limit;
     g.epoch = epoch;
 }
 
-static int pick_tile(int M, int N, bool gated) {
+static int pick_tile(int M, int N, bool gated, int prow = 0) {
     if (g_ctx.tile_override == 1) return kTile256;
     if (g_ctx.tile_override == 2) return kTile128;
-    // Gated operators need several tiles per arriving partition; a plain GEMM
-    // takes the larger tile when it still fills every CU.
-    if (gated) return kTile128;
+    // A plain GEMM takes the larger (faster) tile when it still fills every
+    // CU. Gated operators need several tiles per arriving partition, so they
+    // take it only when the GEMM is at least four waves of 256 x 256 tiles
+    // and a partition spans whole 256-row tiles; below that the 128 x 128
+    // tile's finer granularity wins.
     const long t256 = (long)((M + 255) / 256) * ((N + 255) / 256);
+    if (gated) return (t256 >= 4L * g_ctx.num_cu && prow >= 256 && prow % 256 == 0) ? kTile256 : kTile128;
     return t256 >= g_ctx.num_cu ? kTile256 : kTile128;
 }
 
@@ -715,6 +736,7 @@ static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A,
     g.C = (uint16_t *)C;
     g.P = P;
     g.M = M; g.N = N; g.K = K;
+    g.kslice = K;
     g.lda = K; g.ldw = K; g.ldc = N; g.ldp = N;
     g.a_bytes = (uint32_t)(a_rows * (size_t)K * 2);
     g.w_bytes = (uint32_t)((size_t)N * K * 2);
@@ -734,6 +756,30 @@ static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A,
         g.rt_hi[t] = 0;
     }
     return COMPASS_OK;
+}
+
+// Split K for a launch with too few tiles to occupy every workgroup slot:
+// s slices per tile (at most kMaxSplit, each at least kMinSliceK deep, K
+// slices multiples of 64), s * tiles <= slots, so that every slot gets a
+// slice and the partials fit the workspace.
+static void set_split(GemmParams &g, int cfg) {
+    Ctx &c = g_ctx;
+    const int tiles = g.tiles_m * g.tiles_n;
+    const int slots = g_ctx.grid_override > 0 ? g_ctx.grid_override : c.num_cu * tile_wg_per_cu(cfg);
+    if (!(c.sched & kSchedSplitK) || !c.split_ws || tiles > kMaxSplitTiles || 2 * tiles > slots) return;
+    int sp = std::min(std::min(slots / tiles, kMaxSplit), std::max(1, g.K / kMinSliceK));
+    if (sp < 2) return;
+    const size_t tile_bytes = (size_t)tile_rows(cfg) * tile_cols(cfg) * sizeof(float);
+    while (sp > 1 && (size_t)tiles * sp * tile_bytes > c.split_ws_bytes) --sp;
+    if (sp < 2) return;
+    const int kslice = ((g.K + sp - 1) / sp + 63) / 64 * 64;
+    sp = (g.K + kslice - 1) / kslice;
+    if (sp < 2) return;
+    g.ksplit = sp;
+    g.kslice = kslice;
+    g.grid = std::min(tiles * sp, slots);
+    g.nq = g.grid >= kMaxQueues ? kMaxQueues : 1;
+    g.q_size = std::max(1, g.grid / g.nq);
 }
 
 static void touch_all(GemmParams &g, int nparts) {
@@ -938,7 +984,8 @@ static int launch(const GemmParams &g0, int cfg, bool rs, hipStream_t s) {
         g.tile_trace = c.tile_trace;
         g.trace_base = c.trace_used;
         g.trace_cap = c.trace_cap;
-        c.trace_used = std::min<uint64_t>(c.trace_cap, (uint64_t)c.trace_used + (uint64_t)g0.tiles_m * g0.tiles_n);
+        c.trace_used = std::min<uint64_t>(c.trace_cap,
+                                          (uint64_t)c.trace_used + (uint64_t)g0.tiles_m * g0.tiles_n * g0.ksplit);
     }
     const bool timed = c.timing && c.timed_count < Ctx::kTimed;
     if (timed) hipEventRecord(c.ev_begin[c.timed_count], s);
@@ -1012,7 +1059,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true);
+    const int cfg = pick_tile(p->M, p->N, true, geo.prow);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M);
     g.gate = kGateMain;
@@ -1037,7 +1084,7 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true);
+    const int cfg = pick_tile(p->M, p->N, true, geo.prow);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M);
     g.gate = kGateEpilogue;
@@ -1114,6 +1161,7 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
             for (int q = 0; q < geo.P; ++q)
                 if (g.send_mask & (1ull << q)) g.done_expect[q] = (uint32_t)(g.tiles_m * g.tiles_n);
         }
+        set_split(g, cfg);
     }
     if (p->pattern == COMPASS_AG_GEMM) {
         submit(0, std::move(ag_f));
@@ -1140,6 +1188,7 @@ int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const fl
     const int cfg = pick_tile(M, N, false);
     if ((rc = set_shape(g, cfg, M, N, K, A, M, W, C, P)) != COMPASS_OK) return rc;
     g.gate = kGateNone;
+    set_split(g, cfg);
     return launch(g, cfg, P != nullptr, (hipStream_t)stream);
 }
 
@@ -1189,6 +1238,7 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
     const int cfg = pick_tile(p->M, p->N, false);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
     g.gate = kGateNone;
+    set_split(g, cfg);
     if ((rc = launch(g, cfg, true, s)) != COMPASS_OK) return rc;
     std::vector<int> wait;
     for (int r = 0; r < 2; ++r)
@@ -1277,7 +1327,7 @@ int op_set_option(int key, long long v) {
         return COMPASS_OK;
     }
     case COMPASS_OPT_SCHED:
-        if (v < 0 || v > 3) return set_error(COMPASS_ERR_INVALID, "schedule option must be in [0, 3]");
+        if (v < 0 || v > 7) return set_error(COMPASS_ERR_INVALID, "schedule option must be in [0, 7]");
         c.sched = (int)v;
         return COMPASS_OK;
     case COMPASS_OPT_DROP_FLAG:

@@ -1,0 +1,184 @@
+"""Measurement study around the benchmark step, on one GPU:
+
+    python -m paper_2609_10549_amd.sweep [--out sweep.json] [--quick]
+
+* InterDecom sweep on the QKV-projection shape (AllGather, 4096 tokens,
+  hidden 8192, TP = 8 share N = 3072, single ring): T(d) for
+  d = 1, 2, 4, 8, 16, the fused operator, compass_pick_strategy's choice (with
+  the stored calibration), the measured best d, the regret of the predicted
+  d* and the gap of the fixed d = 4 heuristic (Section V-B, Fig. 8).
+* Overlap at the comp/comm ratios of the paper's Table I (lambda = 0.72,
+  0.89, 4.39, 5.17) and at lambda = 1 for the two MLP operators of the
+  benchmark step (AllGather 8192x2048x4096 double ring, ReduceScatter
+  8192x4096x2048 single ring). A lambda whose link rate the copy engines
+  cannot reach is reported once at the engines' ceiling (unpaced). The
+  compute-dominated ratios (lambda > 2) need more flops per link byte than
+  those shapes have: they are measured on the Table IV shapes with the
+  largest N (AllGather 8192x16384x4096) and the largest K (ReduceScatter
+  8192x4096x16384), as far as the ceiling allows.
+* The GPT-3 175B shapes (8192 tokens, hidden 12288, TP = 8) over a double
+  ring whose directions run at 4 : 1.
+* torch.matmul (hipBLASLt) on every GEMM shape, for context.
+
+Timing only: the inputs are seeded random bf16 on the GPU (parity is the
+tests' job). Every number is the median of several HIP-event-timed calls.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+
+import torch
+
+from . import calibrate as CAL
+from . import compass as C
+
+LAMBDAS = (0.72, 0.89, 1.0, 4.39, 5.17)
+CEILING_FRACTION = 0.95
+
+
+def _fused(pat):
+    return C.compass_ag_gemm if pat == "ag" else C.compass_gemm_rs
+
+
+def _matmul_time(buf, reps=10):
+    A = buf.A.view(torch.bfloat16)
+    B = buf.W.view(torch.bfloat16).t().contiguous()   # K x N, row-major
+    return CAL.time_call(lambda: torch.matmul(A, B), reps=reps)
+
+
+def _pick(pat, M, N, K, n, ring, fwd, bwd, cal):
+    w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+    t = C.compass_topology(ring=C.RINGS[ring], fwd_Bps=fwd, bwd_Bps=bwd, step_latency_s=0.0)
+    return C.compass_pick_strategy(w, t, cal)
+
+
+def overlap_point(buf, pat, lk, tg, reps=7):
+    tx = CAL.time_call(lambda: C.compass_transfer(buf.problem, lk), reps=reps)
+    tf = CAL.time_call(lambda: _fused(pat)(buf.problem, lk), reps=reps)
+    ts = CAL.time_call(lambda: C.compass_sequential(buf.problem, lk), reps=reps)
+    ideal = ts - max(tg, tx)
+    E = (ts - tf) / ideal if ideal > 0 else None
+    h = (tg + tx - tf) / tx
+    return dict(t_xfer_us=tx * 1e6, t_fused_us=tf * 1e6, t_seq_us=ts * 1e6, lam=tg / tx, E=E, h=h)
+
+
+def lambda_study(pat, M, N, K, n, ring, lambdas, verbose):
+    buf = CAL.Buffers(pat, M, N, K, n, ring)
+    tg = CAL.time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P), reps=10)
+    tm = _matmul_time(buf)
+    per_link = CAL.ring_bytes_per_link(pat, M, N, K, n, ring)
+    unpaced = C.links(0.0, 0.0)
+    cap = per_link / CAL.time_call(lambda: C.compass_transfer(buf.problem, unpaced), reps=5)
+    out = dict(pattern=pat, M=M, N=N, K=K, n=n, ring=ring, t_gemm_us=tg * 1e6,
+               gemm_tflops=2.0 * M * N * K / tg / 1e12, torch_matmul_us=tm * 1e6,
+               ceiling_Bps_per_ring=cap, points=[])
+    ceiling_done = False
+    for lam in lambdas:
+        rate = per_link * lam / tg
+        if rate < CEILING_FRACTION * cap:
+            pt = overlap_point(buf, pat, C.links(rate, rate), tg)
+            pt.update(lam_target=lam, rate_Bps=rate)
+        elif not ceiling_done:
+            pt = overlap_point(buf, pat, unpaced, tg)
+            pt.update(lam_target=lam, rate_Bps=0.0, note="rate above the copy-engine ceiling: unpaced")
+            ceiling_done = True
+        else:
+            continue
+        out["points"].append(pt)
+        if verbose:
+            print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in pt.items()}), flush=True)
+    del buf
+    torch.cuda.empty_cache()
+    return out
+
+
+def decomp_study(cal, lam, verbose):
+    pat, M, N, K, n, ring = "ag", 4096, 3072, 8192, 8, "single"
+    buf = CAL.Buffers(pat, M, N, K, n, ring)
+    tg = CAL.time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P), reps=10)
+    per_link = CAL.ring_bytes_per_link(pat, M, N, K, n, ring)
+    unpaced = C.links(0.0, 0.0)
+    cap = per_link / CAL.time_call(lambda: C.compass_transfer(buf.problem, unpaced), reps=5)
+    rate = per_link * lam / tg
+    lk = C.links(rate, rate) if rate < CEILING_FRACTION * cap else unpaced
+    tx = CAL.time_call(lambda: C.compass_transfer(buf.problem, lk), reps=7)
+    times = {}
+    for d in (1, 2, 4, 8, 16):
+        times[d] = CAL.time_call(lambda: C.compass_decomp_gemm(buf.problem, d, lk), reps=7)
+    tf = CAL.time_call(lambda: C.compass_ag_gemm(buf.problem, lk), reps=7)
+    eff = per_link / tx
+    ch = _pick(pat, M, N, K, n, ring, eff, eff, cal)
+    d_meas = min(times, key=times.get)
+    d_star = ch.d_star
+    out = dict(shape=[M, N, K, n, ring], lam_target=lam, rate_Bps=lk.fwd_Bps, t_gemm_us=tg * 1e6,
+               t_xfer_us=tx * 1e6, lam=tg / tx, t_decomp_us={str(d): t * 1e6 for d, t in times.items()},
+               t_fused_us=tf * 1e6, d_meas=d_meas, d_star=d_star,
+               strategy_pick="intra_fusion" if ch.strategy == C.INTRA_FUSION else "inter_decom",
+               strategy_meas="intra_fusion" if tf < times[d_meas] else "inter_decom",
+               regret_d_star=(times[d_star] / times[d_meas] - 1.0) if d_star in times else None,
+               gap_d4=times[4] / times[d_meas] - 1.0,
+               model_t_decomp_us=ch.t_decomp * 1e6, model_t_fusion_us=ch.t_fusion * 1e6)
+    if verbose:
+        print(json.dumps(out), flush=True)
+    del buf
+    torch.cuda.empty_cache()
+    return out
+
+
+def gpt3_study(verbose):
+    """GPT-3 175B shapes, double ring with the forward direction 4x the backward one."""
+    res = []
+    for pat, M, N, K in (("ag", 8192, 6144, 12288), ("rs", 8192, 12288, 6144)):
+        n, ring = 8, "double"
+        buf = CAL.Buffers(pat, M, N, K, n, ring)
+        tg = CAL.time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P), reps=5)
+        tm = _matmul_time(buf, reps=5)
+        per_link = CAL.ring_bytes_per_link(pat, M, N, K, n, ring)
+        unpaced = C.links(0.0, 0.0)
+        cap = per_link / CAL.time_call(lambda: C.compass_transfer(buf.problem, unpaced), reps=3)
+        # the slow direction at the rate that balances the GEMM, capped so the
+        # fast one (4x) stays below the ceiling
+        bwd = min(per_link / tg, CEILING_FRACTION * cap / 4.0)
+        lk = C.links(4.0 * bwd, bwd)
+        pt = overlap_point(buf, pat, lk, tg, reps=5)
+        pt.update(pattern=pat, M=M, N=N, K=K, fwd_Bps=4.0 * bwd, bwd_Bps=bwd, t_gemm_us=tg * 1e6,
+                  gemm_tflops=2.0 * M * N * K / tg / 1e12, torch_matmul_us=tm * 1e6,
+                  fused_tflops=2.0 * M * N * K / (pt["t_fused_us"] * 1e-6) / 1e12)
+        res.append(pt)
+        if verbose:
+            print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in pt.items()}), flush=True)
+        del buf
+        torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=None)
+    ap.add_argument("--quick", action="store_true")
+    args = ap.parse_args()
+    torch.cuda.set_device(0)
+    cal = CAL.load()
+    if cal is None:
+        raise SystemExit("no stored calibration (run python -m paper_2609_10549_amd.calibrate first)")
+    lams = (0.72, 1.0) if args.quick else LAMBDAS
+    result = {"device": torch.cuda.get_device_name(0)}
+    result["decomp"] = [decomp_study(cal, lam, True) for lam in ((1.0,) if args.quick else (0.72, 1.0))]
+    low = tuple(x for x in lams if x <= 2.0)
+    high = tuple(x for x in lams if x > 2.0)
+    result["mlp_fc1_ag"] = lambda_study("ag", 8192, 2048, 4096, 8, "double", low, True)
+    result["mlp_fc2_rs"] = lambda_study("rs", 8192, 4096, 2048, 8, "single", low, True)
+    if high:
+        result["high_lambda_ag"] = lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True)
+        result["high_lambda_rs"] = lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)
+    if not args.quick:
+        result["gpt3_4to1"] = gpt3_study(True)
+    if args.out:
+        with open(args.out, "w") as f:
+            json.dump(result, f, indent=1)
+    print("sweep done", flush=True)
+
+
+if __name__ == "__main__":
+    main()

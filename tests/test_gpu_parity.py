@@ -67,6 +67,62 @@ def test_gemm_with_partial_integer_exact():
     assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref))
 
 
+# ------------------------------------------------------------ split K (few tiles, deep K)
+@pytest.mark.parametrize("with_p", [False, True])
+def test_split_k_integer_exact(with_p):
+    # 2 x 5 tiles of 128 x 128 against 512 workgroup slots: K = 8192 is split
+    M, N, K = 256, 520, 8192
+    _say("split-k int", with_p)
+    if with_p:
+        inp = make_int_rs_inputs(M, N, K, 1, seed=61)
+        A, W = dev_bits(inp["A"]), dev_bits(inp["W"])
+        P = torch.from_numpy(inp["P_in"][0]).cuda()
+        ref = O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]), [inp["P_in"][0].astype(np.float64)], 1)
+    else:
+        inp = make_int_ag_inputs(M, N, K, 1, seed=60)
+        A, W = dev_bits(inp["shards"][0]), dev_bits(inp["W"])
+        P = None
+        ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
+    for rep in range(2):   # the tile counters must be back at zero for the second call
+        Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+        C.compass_gemm(A, W, Cm, P)
+        torch.cuda.synchronize()
+        assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref)), rep
+
+
+def test_split_k_random_close_to_unsplit():
+    M, N, K = 384, 776, 6144
+    inp = make_ag_inputs(M, N, K, 1, seed=62, dist_a=("normal", 1.0), dist_w=("normal", 0.02))
+    A, W = dev_bits(inp["shards"][0]), dev_bits(inp["W"])
+    ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
+    out = {}
+    try:
+        for sched in (7, 3):   # with and without split K
+            C.compass_set_option(C.OPT_SCHED, sched)
+            Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+            C.compass_gemm(A, W, Cm)
+            torch.cuda.synchronize()
+            out[sched] = host_f64(Cm)
+            assert rel_err(out[sched], ref) < TOL, sched
+    finally:
+        C.compass_set_option(C.OPT_SCHED, 7)
+    # both round the same fp32 sums up to ordering: at most one bf16 ulp apart
+    assert rel_err(out[7], out[3]) < 2.0 ** -7
+
+
+def test_decomp_d16_split_integer_exact():
+    # sub-GEMMs of 64 rows: one row tile each, K split
+    n, d = 8, 16
+    M, N, K = 1024, 264, 2048
+    inp = make_int_ag_inputs(M, N, K, n, seed=63)
+    ref = O.f64_to_bf16_rne(O.decomp_ag([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"]), d))
+    case = AGCase(inp, 3, "single")
+    _say("decomp d16 split")
+    C.compass_decomp_gemm(case.problem, d, FAST)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), ref)
+
+
 # ------------------------------------------------------------ fused AllGather+GEMM
 @pytest.mark.parametrize("ring", ["single", "double"])
 @pytest.mark.parametrize("n", [2, 4, 8])
