@@ -92,35 +92,61 @@ def ring_bytes_per_link(pattern, M, N, K, n, ring):
     return (n - 1) * per
 
 
-def run(shapes, ds=(2, 4, 8, 16), lam_targets=(0.5, 1.0, 2.0), ring="double", verbose=True):
-    samples = []
-    rows_out = []
-    for (pat, M, N, K, n) in shapes:
-        buf = Buffers(pat, M, N, K, n, ring)
-        w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
-        tg = time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P))
-        samples.append(C.compass_sample(kind=0, w=w, d=1, t_meas=tg, t_comp=tg, t_comm=0.0))
-        per_link = ring_bytes_per_link(pat, M, N, K, n, ring)
-        for lam in lam_targets:
-            rate = per_link / (tg / lam)
-            lk = C.links(rate, rate)
-            tx = time_call(lambda: C.compass_transfer(buf.problem, lk))
-            tf = time_call(lambda: (C.compass_ag_gemm if pat == "ag" else C.compass_gemm_rs)(buf.problem, lk))
-            samples.append(C.compass_sample(kind=2, w=w, d=1, t_meas=tf, t_comp=tg, t_comm=tx))
-            rec = dict(pattern=pat, M=M, N=N, K=K, n=n, lam_target=lam, rate=rate, t_gemm=tg, t_xfer=tx, t_fused=tf)
-            for d in ds:
-                if (M // n) % (2 * d if ring == "double" else d):
-                    continue
-                td = time_call(lambda: C.compass_decomp_gemm(buf.problem, d, lk))
-                samples.append(C.compass_sample(kind=1, w=w, d=d, t_meas=td, t_comp=tg, t_comm=tx))
-                rec[f"t_decomp_{d}"] = td
-            rows_out.append(rec)
-            if verbose:
-                print(json.dumps(rec), flush=True)
-        del buf
-        torch.cuda.empty_cache()
-    cal = C.compass_calibrate(samples, C.compass_calib(d_max=16))
-    return cal, rows_out
+def measure_shape(shape, ds=(2, 4, 8, 16), lam_targets=(0.5, 1.0, 2.0), ring="double", verbose=True):
+    """Samples of one shape: GEMM alone, and per lambda target the transfer
+    alone, the fused operator and InterDecom at every d that splits it."""
+    pat, M, N, K, n = shape
+    samples, rows_out = [], []
+    buf = Buffers(pat, M, N, K, n, ring)
+    w = dict(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+    tg = time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P))
+    samples.append(dict(kind=0, w=w, d=1, t_meas=tg, t_comp=tg, t_comm=0.0))
+    per_link = ring_bytes_per_link(pat, M, N, K, n, ring)
+    for lam in lam_targets:
+        rate = per_link / (tg / lam)
+        lk = C.links(rate, rate)
+        tx = time_call(lambda: C.compass_transfer(buf.problem, lk))
+        tf = time_call(lambda: (C.compass_ag_gemm if pat == "ag" else C.compass_gemm_rs)(buf.problem, lk))
+        samples.append(dict(kind=2, w=w, d=1, t_meas=tf, t_comp=tg, t_comm=tx))
+        rec = dict(pattern=pat, M=M, N=N, K=K, n=n, lam_target=lam, rate=rate, t_gemm=tg, t_xfer=tx, t_fused=tf)
+        for d in ds:
+            if (M // n) % (2 * d if ring == "double" else d):
+                continue
+            td = time_call(lambda: C.compass_decomp_gemm(buf.problem, d, lk))
+            samples.append(dict(kind=1, w=w, d=d, t_meas=td, t_comp=tg, t_comm=tx))
+            rec[f"t_decomp_{d}"] = td
+        rows_out.append(rec)
+        if verbose:
+            print(json.dumps(rec), flush=True)
+    return samples, rows_out
+
+
+def fit(samples):
+    """compass_calibrate over sample dicts (host only)."""
+    st = [C.compass_sample(kind=x["kind"], w=C.compass_workload(**x["w"]), d=x["d"], t_meas=x["t_meas"],
+                           t_comp=x["t_comp"], t_comm=x["t_comm"]) for x in samples]
+    return C.compass_calibrate(st, C.compass_calib(d_max=16))
+
+
+def run(shapes, verbose=True):
+    """Measure every shape in a child process of its own (a fresh device
+    heap per shape, so that one shape's allocations do not shape the next
+    one's copy speed), then fit."""
+    import subprocess
+    import sys
+    import tempfile
+    samples, rows = [], []
+    for shape in shapes:
+        with tempfile.NamedTemporaryFile(suffix=".json") as tf:
+            rc = subprocess.call([sys.executable, "-u", "-m", "paper_2609_10549_amd.calibrate", "--shape",
+                                  json.dumps(list(shape)), "--out", tf.name] + ([] if verbose else ["--quiet"]))
+            if rc != 0:
+                raise SystemExit(f"calibration of {shape} failed with status {rc}")
+            with open(tf.name) as f:
+                d = json.load(f)
+        samples += d["samples"]
+        rows += d["measurements"]
+    return fit(samples), rows
 
 
 def calib_to_dict(cal) -> dict:
@@ -140,11 +166,23 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=DEFAULT_OUT)
     ap.add_argument("--quick", action="store_true")
+    ap.add_argument("--shape", default=None, help="measure one shape (JSON list) in this process")
+    ap.add_argument("--quiet", action="store_true")
     args = ap.parse_args()
+    if args.shape is not None:
+        torch.cuda.set_device(0)
+        samples, rows = measure_shape(tuple(json.loads(args.shape)), verbose=not args.quiet)
+        with open(args.out, "w") as f:
+            json.dump({"samples": samples, "measurements": rows}, f)
+        return
     cal, rows = run(QUICK if args.quick else SHAPES)
     d = calib_to_dict(cal)
+    import subprocess
+    import sys
+    device = subprocess.run([sys.executable, "-c", "import torch; print(torch.cuda.get_device_name(0))"],
+                            capture_output=True, text=True).stdout.strip()
     with open(args.out, "w") as f:
-        json.dump({"calib": d, "measurements": rows, "device": torch.cuda.get_device_name(0)}, f, indent=1)
+        json.dump({"calib": d, "measurements": rows, "device": device}, f, indent=1)
     print(json.dumps(d))
 
 

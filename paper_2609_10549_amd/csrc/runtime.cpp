@@ -716,17 +716,44 @@ static void init_params(GemmParams &g, uint32_t epoch) {
     g.epoch = epoch;
 }
 
-static int pick_tile(int M, int N, bool gated, int prow = 0) {
+static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.0, bool rs = false) {
     if (g_ctx.tile_override == 1) return kTile256;
     if (g_ctx.tile_override == 2) return kTile128;
+    if (gated && rs) return kTile128;
     // A plain GEMM takes the larger (faster) tile when it still fills every
-    // CU. Gated operators need several tiles per arriving partition, so they
-    // take it only when the GEMM is at least four waves of 256 x 256 tiles
-    // and a partition spans whole 256-row tiles; below that the 128 x 128
-    // tile's finer granularity wins.
+    // CU. The fused AllGather needs several tiles per arriving partition; it
+    // takes it only when a partition spans whole 256-row tiles and the GEMM
+    // is at least four waves of 256 x 256 tiles, or two waves with
+    // computation clearly dominating the transfer (estimated lambda >= 2),
+    // where the larger tile's speed matters more than arrival granularity.
+    // The fused ReduceScatter keeps 128 x 128: with one workgroup per CU its
+    // chunks would finish in bursts of a whole wave, and the sends of all of
+    // them would trail the kernel.
     const long t256 = (long)((M + 255) / 256) * ((N + 255) / 256);
-    if (gated) return (t256 >= 4L * g_ctx.num_cu && prow >= 256 && prow % 256 == 0) ? kTile256 : kTile128;
+    if (gated) {
+        const bool whole = prow >= 256 && prow % 256 == 0;
+        const long cu = g_ctx.num_cu;
+        return whole && (t256 >= 4 * cu || (t256 >= 2 * cu && lam_est >= 2.0)) ? kTile256 : kTile128;
+    }
     return t256 >= g_ctx.num_cu ? kTile256 : kTile128;
+}
+
+// Rough comp/comm ratio of a fused operator, used only to pick its tile: the
+// GEMM at 1 PFLOP/s against the slower ring direction's bytes at its rate
+// (unpaced: that direction's share of the copy engines at the engine model's
+// rate; ReduceScatter incoming gets two thirds of a direction's engines).
+static double lambda_estimate(const compass_problem *p, const Geometry &geo, const compass_links *l) {
+    const double flops = 2.0 * p->M * (double)p->N * p->K;
+    const double step = p->pattern == COMPASS_AG_GEMM ? (double)geo.prow * p->K * 2 : (double)geo.prow * p->N * 4;
+    const bool dbl = p->ring == COMPASS_RING_DOUBLE;
+    double rate = dbl ? std::fmin(l->fwd_Bps, l->bwd_Bps) : l->fwd_Bps;
+    if (!(rate > 0)) {
+        double e = (double)g_ctx.engines.size() / (dbl ? 2.0 : 1.0);
+        if (p->pattern == COMPASS_GEMM_RS) e *= 2.0 / 3.0;
+        rate = e * kEngineBps;
+    }
+    const double t_x = (p->n - 1) * step / rate;
+    return t_x > 0 ? (flops / 1e15) / t_x : 1e9;
 }
 
 static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A, size_t a_rows, const void *W,
@@ -791,7 +818,7 @@ static void touch_all(GemmParams &g, int nparts) {
 
 // Row tiles ordered by the schedule position of the last partition they
 // touch; touched partitions from the identity row map.
-static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M) {
+static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M, bool main_gate) {
     const int bm = tile_rows(cfg);
     std::vector<std::pair<int, int>> key;
     for (int t = 0; t < g.tiles_m; ++t) {
@@ -805,9 +832,13 @@ static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M
     }
     std::stable_sort(key.begin(), key.end());
     for (int i = 0; i < g.tiles_m; ++i) g.rt_order[i] = (uint16_t)key[i].second;
-    // Tiles of one arriving partition are consecutive in the ready order:
-    // short super-blocks deal them out over all XCD queues, and the second
-    // workgroup of each CU waits for the first tickets to go one per CU.
+    // AllGather: the tiles of one arriving partition are consecutive in the
+    // ready order and cannot start before it lands. Short super-blocks deal
+    // them out over all XCD queues, and the second workgroup of each CU
+    // waits for the first tickets to go one per CU. (ReduceScatter tiles
+    // compute before they wait, so they keep the long super-blocks that let
+    // each XCD's L2 reuse its rows of A and W.)
+    if (!main_gate) return;
     if (g_ctx.sched & kSchedFineQueues) g.q_size = std::max(1, g.group_m);
     if ((g_ctx.sched & kSchedSpread) && g.nq == kMaxQueues && g.grid == g_ctx.num_cu * tile_wg_per_cu(cfg) &&
         tile_wg_per_cu(cfg) > 1)
@@ -1059,9 +1090,9 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true, geo.prow);
+    const int cfg = pick_tile(p->M, p->N, true, geo.prow, lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
-    order_by_schedule(g, cfg, geo, p->M);
+    order_by_schedule(g, cfg, geo, p->M, true);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
@@ -1084,9 +1115,9 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true, geo.prow);
+    const int cfg = pick_tile(p->M, p->N, true, geo.prow, lambda_estimate(p, geo, l), true);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
-    order_by_schedule(g, cfg, geo, p->M);
+    order_by_schedule(g, cfg, geo, p->M, false);
     g.gate = kGateEpilogue;
     g.nparts = geo.P;
     g.resident_mask = res;

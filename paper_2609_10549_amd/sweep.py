@@ -153,31 +153,65 @@ def gpt3_study(verbose):
     return res
 
 
+STUDIES = ("decomp", "mlp", "high", "gpt3")
+
+
+def run_study(name, quick, cal):
+    lams = (0.72, 1.0) if quick else LAMBDAS
+    low = tuple(x for x in lams if x <= 2.0)
+    high = tuple(x for x in lams if x > 2.0)
+    if name == "decomp":
+        return {"decomp": [decomp_study(cal, lam, True) for lam in ((1.0,) if quick else (0.72, 1.0))]}
+    if name == "mlp":
+        return {"mlp_fc1_ag": lambda_study("ag", 8192, 2048, 4096, 8, "double", low, True),
+                "mlp_fc2_rs": lambda_study("rs", 8192, 4096, 2048, 8, "single", low, True)}
+    if name == "high":
+        if not high:
+            return {}
+        return {"high_lambda_ag": lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True),
+                "high_lambda_rs": lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)}
+    if name == "gpt3":
+        return {} if quick else {"gpt3_4to1": gpt3_study(True)}
+    raise ValueError(name)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=None)
     ap.add_argument("--quick", action="store_true")
+    ap.add_argument("--only", choices=STUDIES, default=None,
+                    help="run one study in this process (the default runs each in a child process, "
+                         "so that one study's allocations do not shape the next one's memory)")
     args = ap.parse_args()
+    if args.only is None:
+        import subprocess
+        import sys
+        import tempfile
+        result = {}
+        for name in STUDIES:
+            with tempfile.NamedTemporaryFile(suffix=".json") as tf:
+                cmd = [sys.executable, "-u", "-m", "paper_2609_10549_amd.sweep", "--only", name, "--out", tf.name]
+                if args.quick:
+                    cmd.append("--quick")
+                rc = subprocess.call(cmd)
+                if rc != 0:
+                    raise SystemExit(f"study {name} failed with status {rc}")
+                with open(tf.name) as f:
+                    result.update(json.load(f))
+        if args.out:
+            with open(args.out, "w") as f:
+                json.dump(result, f, indent=1)
+        print("sweep done", flush=True)
+        return
     torch.cuda.set_device(0)
     cal = CAL.load()
     if cal is None:
         raise SystemExit("no stored calibration (run python -m paper_2609_10549_amd.calibrate first)")
-    lams = (0.72, 1.0) if args.quick else LAMBDAS
     result = {"device": torch.cuda.get_device_name(0)}
-    result["decomp"] = [decomp_study(cal, lam, True) for lam in ((1.0,) if args.quick else (0.72, 1.0))]
-    low = tuple(x for x in lams if x <= 2.0)
-    high = tuple(x for x in lams if x > 2.0)
-    result["mlp_fc1_ag"] = lambda_study("ag", 8192, 2048, 4096, 8, "double", low, True)
-    result["mlp_fc2_rs"] = lambda_study("rs", 8192, 4096, 2048, 8, "single", low, True)
-    if high:
-        result["high_lambda_ag"] = lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True)
-        result["high_lambda_rs"] = lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)
-    if not args.quick:
-        result["gpt3_4to1"] = gpt3_study(True)
+    result.update(run_study(args.only, args.quick, cal))
     if args.out:
         with open(args.out, "w") as f:
             json.dump(result, f, indent=1)
-    print("sweep done", flush=True)
 
 
 if __name__ == "__main__":
