@@ -395,3 +395,49 @@ def test_kernel_times_one_per_launch():
         assert C.compass_kernel_times() == []   # reading resets
     finally:
         C.compass_set_option(C.OPT_KERNEL_TIMING, 0)
+
+
+# ------------------------------------------------------------ paced links and the tile trace
+def test_paced_link_never_beats_its_rate():
+    # 7 items of 512 KiB per ring direction at 20 GB/s: the last flag is due
+    # after 7 * 512 KiB / rate, and a paced link publishes none earlier
+    n = 8
+    M, N, K = 4096, 64, 1024
+    inp = make_ag_inputs(M, N, K, n, seed=64)
+    case = AGCase(inp, 2, "double")
+    rate = 20e9
+    lk = C.links(rate, rate)
+    C.compass_transfer(case.problem, lk)   # warm
+    C.compass_sync()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    C.compass_transfer(case.problem, lk)
+    b.record()
+    b.synchronize()
+    C.compass_sync()
+    t = a.elapsed_time(b) * 1e-3
+    per_ring = (n - 1) * (M // (2 * n)) * K * 2
+    _say("paced transfer", t, per_ring / rate)
+    assert t >= 0.98 * per_ring / rate
+    assert t < 3.0 * per_ring / rate + 2e-3
+    assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_tile_trace_records_every_work_item():
+    M, N, K = 512, 384, 4096          # 4 x 3 tiles of 128 x 128, K split
+    inp = make_int_ag_inputs(M, N, K, 1, seed=65)
+    A, W = dev_bits(inp["shards"][0]), dev_bits(inp["W"])
+    Cm = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    C.compass_set_option(C.OPT_TILE_TRACE, 4096)
+    try:
+        C.compass_gemm(A, W, Cm)
+        rec = C.compass_tile_trace(4096)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    assert len(rec) >= 12 and len(rec) % 12 == 0          # tiles x K slices
+    assert sorted(rec[:, 0].tolist()) == list(range(len(rec)))
+    t = rec[:, 4:8].astype(np.int64)
+    d = (t[:, 1:] - t[:, :-1]) % (1 << 32)                  # ticket <= gate <= loop <= end
+    assert (d < (1 << 31)).all()
+    ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
+    assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref))
