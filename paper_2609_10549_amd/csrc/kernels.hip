@@ -17,19 +17,18 @@
 //
 // Data path per tile: 4 waves split the tile 2 x 2; each wave holds
 // (BM/2) x (BN/2) fp32 accumulators as 32 x 32 MFMA blocks. A and W stream
-// through LDS with buffer_load ... lds (no register staging; out-of-range
-// rows or K columns read as zero through the buffer bound). Fragment reads
-// of the next MFMA substep are issued between the MFMAs of the current one,
-// and scheduling barriers keep the compiler from sinking them to their use.
-//   256 x 256 (one workgroup per CU): four LDS stages of K = 32 (rows of 64
-//   bytes, 16-byte chunks of row r XOR-permuted by (r >> 2) & 3); loads run
-//   three stages ahead, and the one barrier per stage sits before the last
-//   substep, so the next stage's first fragments are read while that substep
-//   computes.
-//   128 x 128 (two workgroups per CU): two LDS stages of K = 64 (rows of 128
-//   bytes, chunks permuted by (r >> 1) & 7); the next stage's loads go out
-//   in the first two substeps.
-// Either permutation makes a 32-row fragment read hit distinct banks.
+// through two LDS stages of K = 64 (rows of 128 bytes, whole cache lines per
+// load: the texture path's cost grows with the lines a load touches) with
+// buffer_load ... lds (no register staging; out-of-range rows or K columns
+// read as zero through the buffer bound). The one barrier per stage sits
+// before its last substep: by then every wave has read that stage's
+// fragments, so the next-but-one stage's loads may overwrite it, and the next
+// stage's first fragments are read while the last substep computes. Loads of
+// stage s + 1 go out in the last substep of stage s - 1 (A) and the first of
+// stage s (W). Fragment reads of the next substep are issued between the
+// current one's MFMAs; scheduling barriers keep the compiler from sinking
+// them to their use. The 16-byte chunks of LDS row r are XOR-permuted with
+// (r >> 1) & 7, so a 32-row fragment read hits distinct banks.
 //
 // join_kernel: one wave that (optionally) marks the start of a transfer job
 // and waits for a list of flags, putting the end of the copy side onto the
@@ -234,78 +233,50 @@ __device__ __forceinline__ void interleave() {
 
 constexpr int kDsRead = 0x100, kVmemRead = 0x020;
 
-// ---- 256 x 256 pipeline: four stages of K = 32
-constexpr int kBK4 = 32;
+constexpr int kBK = 64;   // K depth of one LDS stage
 
-// One stage on LDS buffers (cA, cW), whose substep-0 fragments are already
-// in (a0, b0). Substep 0: read substep 1's fragments, issue the A loads of
-// stage s + 3 into (dA, ...). Then wait until this wave's loads of stage
-// s + 1 have landed and join the barrier: after it, every wave's loads of
-// stage s + 1 are in LDS and every wave has finished reading the buffer the
-// stage s + 4 loads will overwrite. Substep 1: read stage s + 1's first
-// fragments from (nA, nW), issue the W loads of stage s + 3.
+// ---- the pipeline: two LDS stages of K = 64, barrier before the last substep
+// Stage s on (cA, cW), substep-0 fragments in (a0, b0). Substep 0 issues the
+// W loads of stage s + 1 into (nA, nW) (its A loads went out in stage s - 1);
+// substep 3 waits for all of stage s + 1, joins the barrier, reads stage
+// s + 1's first fragments and issues the A loads of stage s + 2 into
+// (cA, cW), which no wave reads any more.
 template <int BM, int BN, int FM, int FN>
-__device__ __forceinline__ void stage4(const char *cA, const char *cW, const char *nA, const char *nW, char *dA,
-                                       char *dW, f32x16 (&acc)[FN][FM], bf16x8 (&a0)[FM], bf16x8 (&b0)[FN],
-                                       bf16x8 (&a1)[FM], bf16x8 (&b1)[FN], __amdgpu_buffer_rsrc_t rA,
-                                       __amdgpu_buffer_rsrc_t rW, const uint32_t *offA, const uint32_t *offW,
-                                       uint32_t kc2, int r, int swz, int hi, int wm0, int wn0, int wave) {
+__device__ __forceinline__ void stage2e(char *cA, char *cW, char *nA, char *nW, f32x16 (&acc)[FN][FM],
+                                        bf16x8 (&a0)[FM], bf16x8 (&b0)[FN], bf16x8 (&a1)[FM], bf16x8 (&b1)[FN],
+                                        __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rW, const uint32_t *offA,
+                                        const uint32_t *offW, uint32_t kc2_next, uint32_t kc2_next2, int r, int swz,
+                                        int hi, int wm0, int wn0, int wave) {
     constexpr int NM = FM * FN, H = NM / 2, ND = FM + FN;
-    constexpr int LA = BM / 64, LW = BN / 64;   // loads per wave per stage
-    read_frags<FM, FN, 64>(cA, cW, r, swz, 1, hi, wm0, wn0, a1, b1);
+    constexpr int L = BM / 32;   // loads per wave and operand per stage
+    // substep 0
+    read_frags<FM, FN, 128>(cA, cW, r, swz, 1, hi, wm0, wn0, a1, b1);
     mfma_range<0, H, FM, FN>(acc, a0, b0);
     interleave<H, kDsRead, ND>();
-    load_blocks<LA>(rA, dA, offA, 0, kc2, wave);
+    load_blocks<L>(rW, nW, offW, 0, kc2_next, wave);
     mfma_range<H, NM - H, FM, FN>(acc, a0, b0);
-    interleave<NM - H, kVmemRead, LA>();
-    // in flight after this wait: stage s + 2 (LA + LW) and the A half of s + 3
-    wait_vm_lgkm0<LA + LW + LA>();
-    lds_barrier();
-    read_frags<FM, FN, 64>(nA, nW, r, swz, 0, hi, wm0, wn0, a0, b0);
+    interleave<NM - H, kVmemRead, L>();
+    // substep 1
+    read_frags<FM, FN, 128>(cA, cW, r, swz, 2, hi, wm0, wn0, a0, b0);
     mfma_range<0, H, FM, FN>(acc, a1, b1);
     interleave<H, kDsRead, ND>();
-    load_blocks<LW>(rW, dW, offW, 0, kc2, wave);
     mfma_range<H, NM - H, FM, FN>(acc, a1, b1);
-    interleave<NM - H, kVmemRead, LW>();
-}
-
-// ---- 128 x 128 pipeline: two stages of K = 64
-constexpr int kBK2 = 64;
-
-// MFMA substep KK (of 4) of a stage on (sA, sW): read substep KK + 1's
-// fragments between the first half of the MFMAs; in substeps 0 and 1 issue
-// half of the next stage's loads into (dA, dW) between the second half.
-template <int KK, int BM, int BN, int FM, int FN>
-__device__ __forceinline__ void substep2(const char *sA, const char *sW, char *dA, char *dW,
-                                         f32x16 (&acc)[FN][FM], bf16x8 (&a)[2][FM], bf16x8 (&b)[2][FN], bool load,
-                                         __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rW, const uint32_t *offA,
-                                         const uint32_t *offW, uint32_t kc2, int r, int swz, int hi, int wm0, int wn0,
-                                         int wave) {
-    constexpr int cur = KK & 1;
-    constexpr int NM = FM * FN, H = NM / 2, ND = FM + FN;
-    constexpr int LA = (KK < 2) ? BM / 64 : 0, LW = (KK < 2) ? BN / 64 : 0;   // half a stage's loads
-    if constexpr (KK + 1 < 4) read_frags<FM, FN, 128>(sA, sW, r, swz, KK + 1, hi, wm0, wn0, a[cur ^ 1], b[cur ^ 1]);
-    mfma_range<0, H, FM, FN>(acc, a[cur], b[cur]);
-    interleave<H, kDsRead, (KK + 1 < 4) ? ND : 0>();
-    if (load) {
-        load_blocks<LA>(rA, dA, offA, KK * LA, kc2, wave);
-        load_blocks<LW>(rW, dW, offW, KK * LW, kc2, wave);
-    }
-    mfma_range<H, NM - H, FM, FN>(acc, a[cur], b[cur]);
-    interleave<NM - H, kVmemRead, LA + LW>();
-}
-
-template <int BM, int BN, int FM, int FN>
-__device__ __forceinline__ void stage2(const char *sA, const char *sW, char *dA, char *dW, f32x16 (&acc)[FN][FM],
-                                       bool load, __amdgpu_buffer_rsrc_t rA, __amdgpu_buffer_rsrc_t rW,
-                                       const uint32_t *offA, const uint32_t *offW, uint32_t kc2, int r, int swz,
-                                       int hi, int wm0, int wn0, int wave) {
-    bf16x8 a[2][FM], b[2][FN];
-    read_frags<FM, FN, 128>(sA, sW, r, swz, 0, hi, wm0, wn0, a[0], b[0]);
-    substep2<0, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
-    substep2<1, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
-    substep2<2, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
-    substep2<3, BM, BN, FM, FN>(sA, sW, dA, dW, acc, a, b, load, rA, rW, offA, offW, kc2, r, swz, hi, wm0, wn0, wave);
+    interleave<NM - H, kVmemRead, 0>();
+    // substep 2
+    read_frags<FM, FN, 128>(cA, cW, r, swz, 3, hi, wm0, wn0, a1, b1);
+    mfma_range<0, H, FM, FN>(acc, a0, b0);
+    interleave<H, kDsRead, ND>();
+    mfma_range<H, NM - H, FM, FN>(acc, a0, b0);
+    interleave<NM - H, kVmemRead, 0>();
+    // substep 3
+    wait_vm_lgkm0<0>();
+    lds_barrier();
+    read_frags<FM, FN, 128>(nA, nW, r, swz, 0, hi, wm0, wn0, a0, b0);
+    mfma_range<0, H, FM, FN>(acc, a1, b1);
+    interleave<H, kDsRead, ND>();
+    load_blocks<L>(rA, cA, offA, 0, kc2_next2, wave);
+    mfma_range<H, NM - H, FM, FN>(acc, a1, b1);
+    interleave<NM - H, kVmemRead, L>();
 }
 
 // RS = false: optional main-loop gate (AllGather), plain store.
@@ -315,18 +286,12 @@ __global__ __launch_bounds__(kThreads, BM == 256 ? 1 : 2)
 void gemm_kernel(const GemmParams p) {
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr bool P4 = BM == 256;          // four stages of K = 32, else two of K = 64
-    constexpr int ROWB = P4 ? 64 : 128;     // LDS bytes per tile row and stage
-    constexpr int NOFF = P4 ? BM / 64 : BM / 32;   // loads per wave and stage (each operand)
-    static_assert(BM == BN && BM * ROWB == 16384, "both pipelines use 16 KiB per operand stage");
-    __shared__ __attribute__((aligned(1024))) char sA0[BM * ROWB];
-    __shared__ __attribute__((aligned(1024))) char sA1[BM * ROWB];
-    __shared__ __attribute__((aligned(1024))) char sA2[P4 ? BM * ROWB : 16];
-    __shared__ __attribute__((aligned(1024))) char sA3[P4 ? BM * ROWB : 16];
-    __shared__ __attribute__((aligned(1024))) char sW0[BN * ROWB];
-    __shared__ __attribute__((aligned(1024))) char sW1[BN * ROWB];
-    __shared__ __attribute__((aligned(1024))) char sW2[P4 ? BN * ROWB : 16];
-    __shared__ __attribute__((aligned(1024))) char sW3[P4 ? BN * ROWB : 16];
+    constexpr int NOFF = BM / 32;   // loads per wave, operand and stage
+    static_assert(BM == BN && BM * 128 >= 16384, "square tiles; stage buffers hold the epilogue patches");
+    __shared__ __attribute__((aligned(1024))) char sA0[BM * 128];
+    __shared__ __attribute__((aligned(1024))) char sA1[BM * 128];
+    __shared__ __attribute__((aligned(1024))) char sW0[BN * 128];
+    __shared__ __attribute__((aligned(1024))) char sW1[BN * 128];
     __shared__ int s_pos;
     __shared__ int s_ok;
     __shared__ int s_last;
@@ -342,15 +307,14 @@ void gemm_kernel(const GemmParams p) {
     const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, (int)p.w_bytes, 0x00020000);
 
-    // loader geometry. Four stages: block q of this wave holds tile rows
-    // 64 q + 16 wave + (lane >> 2), physical chunk lane & 3. Two stages: rows
-    // 32 q + 8 wave + (lane >> 3), physical chunk lane & 7. A lane loads the
-    // logical chunk that the permutation puts at its physical chunk.
-    const int lrow0 = P4 ? 16 * wave + (lane >> 2) : 8 * wave + (lane >> 3);
-    const int cchunk = P4 ? (lane & 3) ^ ((lane >> 4) & 3) : (lane & 7) ^ ((4 * wave + (lane >> 4)) & 7);
+    // loader geometry: load q of this wave covers tile rows 32 q + 8 wave +
+    // (lane >> 3), 128 bytes (K = 64) each; the lane loads the logical chunk
+    // that the permutation (row >> 1) & 7 puts at its physical chunk lane & 7
+    const int lrow0 = 8 * wave + (lane >> 3);
+    const int cchunk = (lane & 7) ^ ((4 * wave + (lane >> 4)) & 7);
     const int r = lane & 31;                       // fragment row
     const int hi = lane >> 5;                      // fragment K half
-    const int swz = P4 ? (r >> 2) & 3 : (r >> 1) & 7;
+    const int swz = (r >> 1) & 7;
 
     uint64_t known = 0;   // partitions already acquired by this workgroup
     bool failed = false;
@@ -415,63 +379,39 @@ void gemm_kernel(const GemmParams p) {
         {   // a timed-out tile still runs (its loads stay in bounds); only its
             // stores are dropped
             uint32_t offA[NOFF], offW[NOFF];
-            constexpr int RSTEP = BM / NOFF;       // tile rows between a wave's loads
 #pragma unroll
             for (int q = 0; q < NOFF; ++q) {
-                const int ia = m0 + RSTEP * q + lrow0;
+                const int ia = m0 + 32 * q + lrow0;
                 offA[q] = ia < p.M ? (uint32_t)map_row(p, ia) * (uint32_t)p.lda * 2u : kOOB;
-                const int iw = n0 + RSTEP * q + lrow0;
+                const int iw = n0 + 32 * q + lrow0;
                 offW[q] = iw < p.N ? (uint32_t)iw * (uint32_t)p.ldw * 2u : kOOB;
             }
             auto kcol = [&](int st) -> uint32_t {   // byte offset of this lane's K chunk in stage st
-                const int kc = kb + st * (P4 ? kBK4 : kBK2) + cchunk * 8;
+                const int kc = kb + st * kBK + cchunk * 8;
                 return kc < ke ? (uint32_t)kc * 2u : kOOB;
             };
-            // stage counts rounded up so that the unrolled loops have no early
-            // exit (padding stages read only out-of-range columns, i.e. zeros)
-            const int KT4 = (((ke - kb + kBK4 - 1) / kBK4) + 3) & ~3;
-            const int KT2 = (((ke - kb + kBK2 - 1) / kBK2) + 1) & ~1;
-            if constexpr (P4) {
-                constexpr int L = BM / 64;
-                // prologue: stages 0, 1, 2 in flight; stage 0 landed, its first fragments read
-                load_blocks<L>(rA, sA0, offA, 0, kcol(0), wave);
-                load_blocks<L>(rW, sW0, offW, 0, kcol(0), wave);
-                load_blocks<L>(rA, sA1, offA, 0, kcol(1), wave);
-                load_blocks<L>(rW, sW1, offW, 0, kcol(1), wave);
-                load_blocks<L>(rA, sA2, offA, 0, kcol(2), wave);
-                load_blocks<L>(rW, sW2, offW, 0, kcol(2), wave);
-                wait_vm_lgkm0<4 * L>();
-                lds_barrier();
-                bf16x8 a0[FM], b0[FN], a1[FM], b1[FN];
-                read_frags<FM, FN, 64>(sA0, sW0, r, swz, 0, hi, wm0, wn0, a0, b0);
-                for (int st = 0; st < KT4; st += 4) {
-                    stage4<BM, BN, FM, FN>(sA0, sW0, sA1, sW1, sA3, sW3, acc, a0, b0, a1, b1, rA, rW, offA, offW,
-                                           kcol(st + 3), r, swz, hi, wm0, wn0, wave);
-                    stage4<BM, BN, FM, FN>(sA1, sW1, sA2, sW2, sA0, sW0, acc, a0, b0, a1, b1, rA, rW, offA, offW,
-                                           kcol(st + 4), r, swz, hi, wm0, wn0, wave);
-                    stage4<BM, BN, FM, FN>(sA2, sW2, sA3, sW3, sA1, sW1, acc, a0, b0, a1, b1, rA, rW, offA, offW,
-                                           kcol(st + 5), r, swz, hi, wm0, wn0, wave);
-                    stage4<BM, BN, FM, FN>(sA3, sW3, sA0, sW0, sA2, sW2, acc, a0, b0, a1, b1, rA, rW, offA, offW,
-                                           kcol(st + 6), r, swz, hi, wm0, wn0, wave);
-                }
-                // the three stages loaded past the end (zeros) land before the
-                // buffers are reused
-                __builtin_amdgcn_s_waitcnt(0);
-                __syncthreads();
-            } else {
-                load_blocks<NOFF>(rA, sA0, offA, 0, kcol(0), wave);
-                load_blocks<NOFF>(rW, sW0, offW, 0, kcol(0), wave);
-                for (int kt = 0; kt < KT2; kt += 2) {
-                    __builtin_amdgcn_s_waitcnt(0);
-                    __syncthreads();
-                    stage2<BM, BN, FM, FN>(sA0, sW0, sA1, sW1, acc, true, rA, rW, offA, offW, kcol(kt + 1), r, swz,
-                                           hi, wm0, wn0, wave);
-                    __builtin_amdgcn_s_waitcnt(0);
-                    __syncthreads();
-                    stage2<BM, BN, FM, FN>(sA1, sW1, sA0, sW0, acc, kt + 2 < KT2, rA, rW, offA, offW, kcol(kt + 2),
-                                           r, swz, hi, wm0, wn0, wave);
-                }
+            // an even stage count keeps the unrolled loop free of early exits
+            // (padding stages read only out-of-range columns, i.e. zeros)
+            const int KT = (((ke - kb + kBK - 1) / kBK) + 1) & ~1;
+            // prologue: stage 0 and the A half of stage 1 in flight; stage 0
+            // landed, its first fragments read
+            load_blocks<NOFF>(rA, sA0, offA, 0, kcol(0), wave);
+            load_blocks<NOFF>(rW, sW0, offW, 0, kcol(0), wave);
+            load_blocks<NOFF>(rA, sA1, offA, 0, kcol(1), wave);
+            wait_vm_lgkm0<NOFF>();
+            lds_barrier();
+            bf16x8 a0[FM], b0[FN], a1[FM], b1[FN];
+            read_frags<FM, FN, 128>(sA0, sW0, r, swz, 0, hi, wm0, wn0, a0, b0);
+            for (int st = 0; st < KT; st += 2) {
+                stage2e<BM, BN, FM, FN>(sA0, sW0, sA1, sW1, acc, a0, b0, a1, b1, rA, rW, offA, offW, kcol(st + 1),
+                                        kcol(st + 2), r, swz, hi, wm0, wn0, wave);
+                stage2e<BM, BN, FM, FN>(sA1, sW1, sA0, sW0, acc, a0, b0, a1, b1, rA, rW, offA, offW, kcol(st + 2),
+                                        kcol(st + 3), r, swz, hi, wm0, wn0, wave);
             }
+            // the loads issued past the end (zeros) land before the buffers
+            // are reused
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
         }
 
         if (traced && tid == 0) t_loop = rtc32();
