@@ -454,11 +454,11 @@ void gemm_kernel(const GemmParams p) {
         const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
         // bf16 store of 4 values at tile (row, col), after adding the fp32
         // partial sum (ReduceScatter): 64 contiguous bytes of C per row
-        auto store4 = [&](int row, int col, float v0, float v1, float v2, float v3) {
+        auto store4 = [&](int row, int col, float v0, float v1, float v2, float v3, bool add_p) {
             const int m = m0 + row, n = n0 + col;
             if (m < mlim && n < p.N) {
                 const int pm = map_row(p, m);
-                if (RS && p.P) {
+                if (add_p) {
                     const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
                     v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
                 }
@@ -468,6 +468,7 @@ void gemm_kernel(const GemmParams p) {
                 *reinterpret_cast<uint2 *>(p.C + (size_t)pm * p.ldc + n) = o;
             }
         };
+        const bool has_p = RS && p.P != nullptr;
 
         // split K: every slice stores its partial tile (fp32, row-major);
         // the slice that completes the tile's count sums all of them in
@@ -523,10 +524,53 @@ void gemm_kernel(const GemmParams p) {
                             sum[0] += part[jj][0]; sum[1] += part[jj][1];
                             sum[2] += part[jj][2]; sum[3] += part[jj][3];
                         }
-                    store4(row, col, sum[0], sum[1], sum[2], sum[3]);
+                    store4(row, col, sum[0], sum[1], sum[2], sum[3], has_p);
+                }
+            } else if (BM == 256 && has_p) {
+                // as through_patch, with each block's fp32 partial loaded PD
+                // blocks ahead of its use (one block at a time would expose a
+                // memory latency per block; the 128 x 128 tile, whose
+                // accumulators share the register file, has no room for it)
+                constexpr int NB = FM * FN, PD = 2, NBUF = PD + 1;
+                const int rr = lane >> 3, rc = lane & 7;
+                f32x4 pb[NBUF][4];
+                auto load_p = [&](int blk, f32x4 (&dst)[4]) {
+                    const int mi = blk / FN, ni = blk % FN;
+#pragma unroll
+                    for (int it = 0; it < 4; ++it) {
+                        const int m = m0 + wm0 + mi * 32 + rr + 8 * it;
+                        const int n = n0 + wn0 + ni * 32 + 4 * rc;
+                        dst[it] = (m < p.M && n < p.N)
+                                      ? *reinterpret_cast<const f32x4 *>(p.P + (size_t)map_row(p, m) * p.ldp + n)
+                                      : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                    }
+                };
+#pragma unroll
+                for (int blk = 0; blk < PD && blk < NB; ++blk) load_p(blk, pb[blk]);
+#pragma unroll
+                for (int blk = 0; blk < NB; ++blk) {
+                    if (blk + PD < NB) load_p(blk + PD, pb[(blk + PD) % NBUF]);
+                    const int mi = blk / FN, ni = blk % FN;
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int cc = 2 * g + hi;
+                        f32x4 v4 = {acc[ni][mi][4 * g + 0], acc[ni][mi][4 * g + 1],
+                                    acc[ni][mi][4 * g + 2], acc[ni][mi][4 * g + 3]};
+                        *reinterpret_cast<f32x4 *>(patch + r * 128 + ((cc ^ (r & 7)) << 4)) = v4;
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): patch written
+#pragma unroll
+                    for (int it = 0; it < 4; ++it) {
+                        const int row = rr + 8 * it;
+                        const f32x4 x = *reinterpret_cast<const f32x4 *>(patch + row * 128 + ((rc ^ (row & 7)) << 4));
+                        const f32x4 pv = pb[blk % NBUF][it];
+                        store4(wm0 + mi * 32 + row, wn0 + ni * 32 + 4 * rc, x[0] + pv[0], x[1] + pv[1],
+                               x[2] + pv[2], x[3] + pv[3], false);
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // patch read before reuse
                 }
             } else {
-                through_patch([&](int row, int col, f32x4 x) { store4(row, col, x[0], x[1], x[2], x[3]); });
+                through_patch([&](int row, int col, f32x4 x) { store4(row, col, x[0], x[1], x[2], x[3], has_p); });
             }
         }
 
