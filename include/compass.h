@@ -240,7 +240,8 @@ int compass_kernel_times(double *us, int cap);
  * launch's ready order: [0] position, [1] row tile << 16 | column tile,
  * [2] HW_ID and [3] XCC_ID of the workgroup that ran it, [4..7] the GPU's
  * 100 MHz real-time counter (low 32 bits) when the workgroup took the ticket,
- * passed the arrival gate, left the main loop and finished the epilogue. */
+ * passed the arrival gate (ReduceScatter: the epilogue's gate, so [5] comes
+ * after [6]), left the main loop and finished the epilogue. */
 int compass_tile_trace(uint32_t *records, int cap);
 
 /* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */

@@ -366,7 +366,7 @@ void gemm_kernel(const GemmParams p) {
             if (!s_ok) failed = true;
             known |= need;
         }
-        if (traced && tid == 0) t_gate = rtc32();
+        if (!RS && traced && tid == 0) t_gate = rtc32();
 
         f32x16 acc[FN][FM];
 #pragma unroll
@@ -452,6 +452,10 @@ void gemm_kernel(const GemmParams p) {
             }
         };
         const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
+        // a tile of a chunk that is sent on (ReduceScatter) stores with
+        // system-scope write-through, so that no L2 write-back is needed
+        // before the copy engines read it
+        const bool wt = RS && p.done_host != nullptr && (touch & p.send_mask) != 0;
         // bf16 store of 4 values at tile (row, col), after adding the fp32
         // partial sum (ReduceScatter): 64 contiguous bytes of C per row
         auto store4 = [&](int row, int col, float v0, float v1, float v2, float v3, bool add_p) {
@@ -462,10 +466,12 @@ void gemm_kernel(const GemmParams p) {
                     const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
                     v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
                 }
-                uint2 o;
-                o.x = pack_bf16x2(v0, v1);
-                o.y = pack_bf16x2(v2, v3);
-                *reinterpret_cast<uint2 *>(p.C + (size_t)pm * p.ldc + n) = o;
+                const uint64_t o = (uint64_t)pack_bf16x2(v0, v1) | ((uint64_t)pack_bf16x2(v2, v3) << 32);
+                uint64_t *dst = reinterpret_cast<uint64_t *>(p.C + (size_t)pm * p.ldc + n);
+                if (wt)   // written through to memory: the copy engines read it
+                    __hip_atomic_store(dst, o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                else
+                    *dst = o;
             }
         };
         const bool has_p = RS && p.P != nullptr;
@@ -505,6 +511,7 @@ void gemm_kernel(const GemmParams p) {
             if (!s_ok) failed = true;
             known |= need;
         }
+        if (RS && traced && tid == 0) t_gate = rtc32();
 
         if (finish) {
             if (p.ksplit > 1) {
@@ -574,11 +581,11 @@ void gemm_kernel(const GemmParams p) {
             }
         }
 
+        if (wt) __builtin_amdgcn_s_waitcnt(0);   // write-through stores acknowledged
         __syncthreads();   // stores issued and complete; LDS free for the next tile
         if (RS && finish && p.done_host && !failed && tid == 0) {
             uint64_t dm = touch & p.send_mask;
             if (dm) {
-                __threadfence_system();   // tile data written back before counting
                 while (dm) {
                     const int q = __builtin_ctzll(dm);
                     const uint32_t old = __hip_atomic_fetch_add(&p.done_cnt[p.flag_base + q], 1u,
