@@ -40,6 +40,7 @@ struct GemmParams {
     const float *P;      // fp32 partial added before rounding (or null)
     uint32_t a_bytes;    // extent of A in bytes (buffer bound)
     uint32_t w_bytes;    // extent of W in bytes
+    uint32_t p_bytes;    // extent of P in bytes (buffer bound of the partial loads)
     int M, N, K;         // logical rows of this launch, columns, depth
     int lda, ldw, ldc, ldp;
     int tiles_m, tiles_n;

@@ -533,30 +533,35 @@ void gemm_kernel(const GemmParams p) {
                         }
                     store4(row, col, sum[0], sum[1], sum[2], sum[3], has_p);
                 }
-            } else if (BM == 256 && has_p) {
-                // as through_patch, with each block's fp32 partial loaded PD
-                // blocks ahead of its use (one block at a time would expose a
-                // memory latency per block; the 128 x 128 tile, whose
-                // accumulators share the register file, has no room for it)
-                constexpr int NB = FM * FN, PD = 2, NBUF = PD + 1;
+            } else if (has_p) {
+                // as through_patch, with each 32 x 32 block's fp32 partial
+                // brought into LDS by buffer_load ... lds one block ahead of
+                // its use (two 4 KiB buffers per wave in the freed stage
+                // buffers; loading it into registers one block at a time
+                // would expose a memory latency per block)
+                constexpr int NB = FM * FN;
+                const __amdgpu_buffer_rsrc_t rP =
+                    __builtin_amdgcn_make_buffer_rsrc((void *)p.P, (short)0, (int)p.p_bytes, 0x00020000);
                 const int rr = lane >> 3, rc = lane & 7;
-                f32x4 pb[NBUF][4];
-                auto load_p = [&](int blk, f32x4 (&dst)[4]) {
+                char *pbuf0 = sA1 + wave * 4096;
+                char *pbuf1 = sW0 + wave * 4096;
+                auto load_p = [&](int blk, char *dst) {
                     const int mi = blk / FN, ni = blk % FN;
+                    const int n = n0 + wn0 + ni * 32 + 4 * rc;
 #pragma unroll
                     for (int it = 0; it < 4; ++it) {
                         const int m = m0 + wm0 + mi * 32 + rr + 8 * it;
-                        const int n = n0 + wn0 + ni * 32 + 4 * rc;
-                        dst[it] = (m < p.M && n < p.N)
-                                      ? *reinterpret_cast<const f32x4 *>(p.P + (size_t)map_row(p, m) * p.ldp + n)
-                                      : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                        const uint32_t off = (m < p.M && n < p.N)
+                                                 ? ((uint32_t)map_row(p, m) * (uint32_t)p.ldp + (uint32_t)n) * 4u
+                                                 : 0x80000000u;
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rP, LDS_AS(dst + it * 1024), 16, off, 0, 0, 0);
                     }
                 };
-#pragma unroll
-                for (int blk = 0; blk < PD && blk < NB; ++blk) load_p(blk, pb[blk]);
+                load_p(0, pbuf0);
 #pragma unroll
                 for (int blk = 0; blk < NB; ++blk) {
-                    if (blk + PD < NB) load_p(blk + PD, pb[(blk + PD) % NBUF]);
+                    char *pcur = (blk & 1) ? pbuf1 : pbuf0;
+                    if (blk + 1 < NB) load_p(blk + 1, (blk & 1) ? pbuf0 : pbuf1);
                     const int mi = blk / FN, ni = blk % FN;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
@@ -570,11 +575,11 @@ void gemm_kernel(const GemmParams p) {
                     for (int it = 0; it < 4; ++it) {
                         const int row = rr + 8 * it;
                         const f32x4 x = *reinterpret_cast<const f32x4 *>(patch + row * 128 + ((rc ^ (row & 7)) << 4));
-                        const f32x4 pv = pb[blk % NBUF][it];
+                        const f32x4 pv = *reinterpret_cast<const f32x4 *>(pcur + row * 128 + rc * 16);
                         store4(wm0 + mi * 32 + row, wn0 + ni * 32 + 4 * rc, x[0] + pv[0], x[1] + pv[1],
                                x[2] + pv[2], x[3] + pv[3], false);
                     }
-                    __builtin_amdgcn_s_waitcnt(0xC07F);   // patch read before reuse
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // patch and partial read before reuse
                 }
             } else {
                 through_patch([&](int row, int col, f32x4 x) { store4(row, col, x[0], x[1], x[2], x[3], has_p); });

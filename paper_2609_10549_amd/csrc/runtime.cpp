@@ -767,6 +767,7 @@ static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A,
     g.lda = K; g.ldw = K; g.ldc = N; g.ldp = N;
     g.a_bytes = (uint32_t)(a_rows * (size_t)K * 2);
     g.w_bytes = (uint32_t)((size_t)N * K * 2);
+    g.p_bytes = P ? (uint32_t)(a_rows * (size_t)N * 4) : 0u;
     const int bm = tile_rows(cfg), bn = tile_cols(cfg);
     g.tiles_m = (M + bm - 1) / bm;
     g.tiles_n = (N + bn - 1) / bn;
