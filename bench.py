@@ -212,11 +212,19 @@ def main():
         return
 
     # ---------------------------------------------------------------- overlap efficiency (untimed region)
+    # GEMM alone, transfer alone, unfused and fused, timed in interleaved
+    # rounds so that the differences the metrics take see one clock state
     say("bench: unfused and fused references")
-    t_seq1 = CAL.time_call(lambda: C.compass_sequential(p_ag, lk1), reps=5)
-    t_seq2 = CAL.time_call(lambda: C.compass_sequential(p_rs, lk2), reps=5)
-    t_fus1 = CAL.time_call(lambda: C.compass_ag_gemm(p_ag, lk1), reps=5)
-    t_fus2 = CAL.time_call(lambda: C.compass_gemm_rs(p_rs, lk2), reps=5)
+    r1 = CAL.time_interleaved({"g": lambda: C.compass_gemm(gathered, W1, C1),
+                               "x": lambda: C.compass_transfer(p_ag, lk1),
+                               "s": lambda: C.compass_sequential(p_ag, lk1),
+                               "f": lambda: C.compass_ag_gemm(p_ag, lk1)})
+    r2 = CAL.time_interleaved({"g": lambda: C.compass_gemm(A2, W2, C2, stage),
+                               "x": lambda: C.compass_transfer(p_rs, lk2),
+                               "s": lambda: C.compass_sequential(p_rs, lk2),
+                               "f": lambda: C.compass_gemm_rs(p_rs, lk2)})
+    t_gemm1, t_x1, t_seq1, t_fus1 = r1["g"], r1["x"], r1["s"], r1["f"]
+    t_gemm2, t_x2, t_seq2, t_fus2 = r2["g"], r2["x"], r2["s"], r2["f"]
 
     def overlap(t_unf, t_fus, tg, tx):
         ideal = t_unf - max(tg, tx)

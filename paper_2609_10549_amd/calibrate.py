@@ -16,6 +16,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import time
 import os
 
 import numpy as np
@@ -67,10 +68,19 @@ class Buffers:
             self.P = self.stage
 
 
-def time_call(fn, reps=5, warmup=2) -> float:
-    """Median seconds of fn() measured with HIP events on the current stream."""
-    for _ in range(warmup):
+def time_call(fn, reps=5, warmup=2, min_warm_s=0.1) -> float:
+    """Median seconds of fn() measured with HIP events on the current stream,
+    after at least `warmup` calls and `min_warm_s` seconds of them (a GPU
+    that was idle runs a millisecond-long GEMM 10-15 % slower for its first
+    few milliseconds of work)."""
+    t0 = time.perf_counter()
+    done = 0
+    while done < warmup or time.perf_counter() - t0 < min_warm_s:
         fn()
+        done += 1
+        if done >= warmup:
+            C.compass_sync()
+            torch.cuda.synchronize()
     C.compass_sync()
     out = []
     for _ in range(reps):
@@ -83,6 +93,32 @@ def time_call(fn, reps=5, warmup=2) -> float:
         out.append(a.elapsed_time(b) * 1e-3)
     C.compass_sync()
     return float(np.median(out))
+
+
+def time_interleaved(fns: dict, reps=7, min_warm_s=0.1) -> dict:
+    """Median seconds of each fn() in `fns`, timed in rounds that call every
+    one of them once, so that all see the same clock and thermal state (the
+    overlap metrics divide differences of these times)."""
+    t0 = time.perf_counter()
+    while True:
+        for fn in fns.values():
+            fn()
+        C.compass_sync()
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= min_warm_s:
+            break
+    out = {k: [] for k in fns}
+    for _ in range(reps):
+        for k, fn in fns.items():
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            out[k].append(a.elapsed_time(b) * 1e-3)
+    C.compass_sync()
+    return {k: float(np.median(v)) for k, v in out.items()}
 
 
 def ring_bytes_per_link(pattern, M, N, K, n, ring):

@@ -719,20 +719,22 @@ static void init_params(GemmParams &g, uint32_t epoch) {
 static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.0, bool rs = false) {
     if (g_ctx.tile_override == 1) return kTile256;
     if (g_ctx.tile_override == 2) return kTile128;
-    if (gated && rs) return kTile128;
     // A plain GEMM takes the larger (faster) tile when it still fills every
     // CU. The fused AllGather needs several tiles per arriving partition; it
     // takes it only when a partition spans whole 256-row tiles and the GEMM
     // is at least four waves of 256 x 256 tiles, or two waves with
     // computation clearly dominating the transfer (estimated lambda >= 2),
     // where the larger tile's speed matters more than arrival granularity.
-    // The fused ReduceScatter keeps 128 x 128: with one workgroup per CU its
-    // chunks would finish in bursts of a whole wave, and the sends of all of
-    // them would trail the kernel.
+    // The fused ReduceScatter takes 256 x 256 only when computation dominates
+    // (estimated lambda >= 1) over at least two waves: with one workgroup per
+    // CU its chunks finish in bursts of a whole wave and the sends of the last
+    // burst trail the kernel, which the faster GEMM repays only when the
+    // transfer is the smaller part.
     const long t256 = (long)((M + 255) / 256) * ((N + 255) / 256);
     if (gated) {
         const bool whole = prow >= 256 && prow % 256 == 0;
         const long cu = g_ctx.num_cu;
+        if (rs) return whole && t256 >= 2 * cu && lam_est >= 1.0 ? kTile256 : kTile128;
         return whole && (t256 >= 4 * cu || (t256 >= 2 * cu && lam_est >= 2.0)) ? kTile256 : kTile128;
     }
     return t256 >= g_ctx.num_cu ? kTile256 : kTile128;

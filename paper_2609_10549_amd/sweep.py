@@ -53,14 +53,17 @@ def _pick(pat, M, N, K, n, ring, fwd, bwd, cal):
     return C.compass_pick_strategy(w, t, cal)
 
 
-def overlap_point(buf, pat, lk, tg, reps=7):
-    tx = CAL.time_call(lambda: C.compass_transfer(buf.problem, lk), reps=reps)
-    tf = CAL.time_call(lambda: _fused(pat)(buf.problem, lk), reps=reps)
-    ts = CAL.time_call(lambda: C.compass_sequential(buf.problem, lk), reps=reps)
+def overlap_point(buf, pat, lk, reps=7):
+    t = CAL.time_interleaved({"g": lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P),
+                              "x": lambda: C.compass_transfer(buf.problem, lk),
+                              "f": lambda: _fused(pat)(buf.problem, lk),
+                              "s": lambda: C.compass_sequential(buf.problem, lk)}, reps=reps)
+    tg, tx, tf, ts = t["g"], t["x"], t["f"], t["s"]
     ideal = ts - max(tg, tx)
     E = (ts - tf) / ideal if ideal > 0 else None
     h = (tg + tx - tf) / tx
-    return dict(t_xfer_us=tx * 1e6, t_fused_us=tf * 1e6, t_seq_us=ts * 1e6, lam=tg / tx, E=E, h=h)
+    return dict(t_gemm_us=tg * 1e6, t_xfer_us=tx * 1e6, t_fused_us=tf * 1e6, t_seq_us=ts * 1e6, lam=tg / tx,
+                E=E, h=h)
 
 
 def lambda_study(pat, M, N, K, n, ring, lambdas, verbose):
@@ -77,10 +80,10 @@ def lambda_study(pat, M, N, K, n, ring, lambdas, verbose):
     for lam in lambdas:
         rate = per_link * lam / tg
         if rate < CEILING_FRACTION * cap:
-            pt = overlap_point(buf, pat, C.links(rate, rate), tg)
+            pt = overlap_point(buf, pat, C.links(rate, rate))
             pt.update(lam_target=lam, rate_Bps=rate)
         elif not ceiling_done:
-            pt = overlap_point(buf, pat, unpaced, tg)
+            pt = overlap_point(buf, pat, unpaced)
             pt.update(lam_target=lam, rate_Bps=0.0, note="rate above the copy-engine ceiling: unpaced")
             ceiling_done = True
         else:
@@ -102,11 +105,14 @@ def decomp_study(cal, lam, verbose):
     cap = per_link / CAL.time_call(lambda: C.compass_transfer(buf.problem, unpaced), reps=5)
     rate = per_link * lam / tg
     lk = C.links(rate, rate) if rate < CEILING_FRACTION * cap else unpaced
-    tx = CAL.time_call(lambda: C.compass_transfer(buf.problem, lk), reps=7)
-    times = {}
+    fns = {"g": lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P),
+           "x": lambda: C.compass_transfer(buf.problem, lk),
+           "f": lambda: C.compass_ag_gemm(buf.problem, lk)}
     for d in (1, 2, 4, 8, 16):
-        times[d] = CAL.time_call(lambda: C.compass_decomp_gemm(buf.problem, d, lk), reps=7)
-    tf = CAL.time_call(lambda: C.compass_ag_gemm(buf.problem, lk), reps=7)
+        fns[d] = (lambda d=d: C.compass_decomp_gemm(buf.problem, d, lk))
+    t = CAL.time_interleaved(fns, reps=7)
+    tg, tx, tf = t["g"], t["x"], t["f"]
+    times = {d: t[d] for d in (1, 2, 4, 8, 16)}
     eff = per_link / tx
     ch = _pick(pat, M, N, K, n, ring, eff, eff, cal)
     d_meas = min(times, key=times.get)
@@ -126,10 +132,14 @@ def decomp_study(cal, lam, verbose):
     return out
 
 
-def gpt3_study(verbose):
+GPT3_SHAPES = {"ag": (8192, 6144, 12288), "rs": (8192, 12288, 6144)}
+
+
+def gpt3_study(pats, verbose):
     """GPT-3 175B shapes, double ring with the forward direction 4x the backward one."""
     res = []
-    for pat, M, N, K in (("ag", 8192, 6144, 12288), ("rs", 8192, 12288, 6144)):
+    for pat in pats:
+        M, N, K = GPT3_SHAPES[pat]
         n, ring = 8, "double"
         buf = CAL.Buffers(pat, M, N, K, n, ring)
         tg = CAL.time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P), reps=5)
@@ -141,9 +151,9 @@ def gpt3_study(verbose):
         # fast one (4x) stays below the ceiling
         bwd = min(per_link / tg, CEILING_FRACTION * cap / 4.0)
         lk = C.links(4.0 * bwd, bwd)
-        pt = overlap_point(buf, pat, lk, tg, reps=5)
-        pt.update(pattern=pat, M=M, N=N, K=K, fwd_Bps=4.0 * bwd, bwd_Bps=bwd, t_gemm_us=tg * 1e6,
-                  gemm_tflops=2.0 * M * N * K / tg / 1e12, torch_matmul_us=tm * 1e6,
+        pt = overlap_point(buf, pat, lk, reps=5)
+        pt.update(pattern=pat, M=M, N=N, K=K, fwd_Bps=4.0 * bwd, bwd_Bps=bwd,
+                  gemm_tflops=2.0 * M * N * K / (pt["t_gemm_us"] * 1e-6) / 1e12, torch_matmul_us=tm * 1e6,
                   fused_tflops=2.0 * M * N * K / (pt["t_fused_us"] * 1e-6) / 1e12)
         res.append(pt)
         if verbose:
@@ -153,7 +163,7 @@ def gpt3_study(verbose):
     return res
 
 
-STUDIES = ("decomp", "mlp", "high", "gpt3")
+STUDIES = ("decomp", "mlp", "high", "gpt3_ag", "gpt3_rs")
 
 
 def run_study(name, quick, cal):
@@ -170,8 +180,9 @@ def run_study(name, quick, cal):
             return {}
         return {"high_lambda_ag": lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True),
                 "high_lambda_rs": lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)}
-    if name == "gpt3":
-        return {} if quick else {"gpt3_4to1": gpt3_study(True)}
+    if name.startswith("gpt3_"):
+        pat = name[len("gpt3_"):]
+        return {} if quick else {f"gpt3_4to1_{pat}": gpt3_study((pat,), True)}
     raise ValueError(name)
 
 

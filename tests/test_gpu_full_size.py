@@ -132,3 +132,21 @@ def test_config5_double_ring_4_to_1_full_size(pattern):
         C.compass_gemm_rs(case.problem, LINKS_4_TO_1)
         C.compass_sync()
         check_rs(case, inp, 2 * inp["n"], seed=502)
+
+
+def test_config5_reducescatter_unpaced_takes_256_tiles():
+    # Unpaced links make the GPT-3 ReduceScatter computation-dominated
+    # (estimated lambda > 1), where the operator takes 256 x 256 tiles: the
+    # tile trace holds one record per output tile, 32 x 48 of them.
+    inp = inputs(5, "rs")
+    case = RSCase(inp, 0, "double")
+    _say("config 5: rs unpaced, tile trace")
+    C.compass_set_option(C.OPT_TILE_TRACE, 8192)
+    try:
+        C.compass_gemm_rs(case.problem, UNPACED)
+        C.compass_sync()
+        rec = C.compass_tile_trace(8192)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    assert len(rec) == (inp["M"] // 256) * (inp["N"] // 256)
+    check_rs(case, inp, 2 * inp["n"], seed=503)
