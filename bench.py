@@ -193,9 +193,18 @@ def main():
         dom = dict(name=f"gemm_kernel, fc2 ReduceScatter ({s2}, d={d2})", flops=flops2 / d2,
                    t=float(np.mean(k2)) * 1e-6, tag="rs")
     achieved = dom["flops"] / dom["t"] / 1e12
+    # context for the fraction: the matrix cores' sustained bf16 rate with no
+    # memory traffic (the clock drops below its 2.4 GHz maximum under load),
+    # and the transfer-alone time that bounds a fused operator at lambda < 1
+    C.compass_probe_mfma(8192)
+    probe_tf, probe_ghz = C.compass_probe_mfma(65536)
+    t_link = t_x1 if dom["tag"] == "ag" else t_x2
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": stored_traffic(dom["tag"]),
-                "kernel": dom["name"], "kernel_us": round(dom["t"] * 1e6, 2)}
+                "kernel": dom["name"], "kernel_us": round(dom["t"] * 1e6, 2),
+                "peak_sustained_probe": round(probe_tf, 1), "sclk_GHz_probe": round(probe_ghz, 3),
+                "frac_of_sustained": round(achieved / probe_tf, 4),
+                "link_floor_us": round(t_link * 1e6, 2), "link_floor_over_kernel": round(t_link / dom["t"], 4)}
 
     result = {
         "metric": "AG-GEMM/GEMM-RS TFLOP/s + overlap efficiency vs unfused GEMM+copy, 1 GPU",

@@ -244,6 +244,18 @@ int compass_kernel_times(double *us, int cap);
  * after [6]), left the main loop and finished the epilogue. */
 int compass_tile_trace(uint32_t *records, int cap);
 
+/* Matrix-core probe (roofline context: the bf16 peak the chip sustains under
+ * load, against the nominal one at the maximum clock). Launches one
+ * workgroup of 8 waves per CU on the null stream; every wave issues `iters`
+ * rounds of 8 independent v_mfma_f32_32x32x16_bf16 (no memory traffic) and
+ * reads the shader-clock and 100 MHz real-time counters around them.
+ * Synchronizes. On success writes the achieved bf16 TFLOP/s over the
+ * kernel's event time to *tflops and the mean shader clock during the loop,
+ * GHz, to *sclk_ghz. iters must lie in [1, 2^22] (about 1 ms per 4096);
+ * COMPASS_ERR_INVALID otherwise or on a null pointer. The library allocates
+ * a small result buffer on the first call and keeps it. */
+int compass_probe_mfma(int iters, double *tflops, double *sclk_ghz);
+
 /* ---- analytic model and selector (Section IV, Section V, Algorithm 1) ---- */
 typedef struct compass_workload {   /* W of Eq. 1 / Eq. 6 */
     int pattern;                    /* COMPASS_AG_GEMM or COMPASS_GEMM_RS     */

@@ -14,6 +14,7 @@ from .compass import (  # noqa: F401
     compass_gemm_rs,
     compass_kernel_times,
     compass_tile_trace,
+    compass_probe_mfma,
     compass_last_error,
     compass_model_t_decomp,
     compass_model_t_fusion,

@@ -108,6 +108,7 @@ _SIGS = {
     "compass_sync": (ctypes.c_int, []),
     "compass_kernel_times": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
     "compass_tile_trace": (ctypes.c_int, [ctypes.POINTER(ctypes.c_uint32), ctypes.c_int]),
+    "compass_probe_mfma": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "compass_set_option": (ctypes.c_int, [ctypes.c_int, ctypes.c_longlong]),
     "compass_pick_strategy": (ctypes.c_int, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology),
                                              ctypes.POINTER(compass_calib), ctypes.POINTER(compass_choice)]),
@@ -272,6 +273,13 @@ def compass_tile_trace(cap: int = 1 << 16):
     k = _check(lib().compass_tile_trace(out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32)), cap),
                "compass_tile_trace")
     return out[:k]
+
+
+def compass_probe_mfma(iters: int = 16384) -> tuple:
+    """(bf16 TFLOP/s, shader clock GHz) of the matrix-core probe; see the header."""
+    tf, ghz = ctypes.c_double(), ctypes.c_double()
+    _check(lib().compass_probe_mfma(iters, ctypes.byref(tf), ctypes.byref(ghz)), "compass_probe_mfma")
+    return tf.value, ghz.value
 
 
 def compass_set_option(key: int, value: int) -> None:

@@ -42,6 +42,10 @@ int compass_kernel_times(double *us, int cap) { return op_kernel_times(us, cap);
 
 int compass_tile_trace(uint32_t *records, int cap) { return op_tile_trace(records, cap); }
 
+int compass_probe_mfma(int iters, double *tflops, double *sclk_ghz) {
+    return op_probe_mfma(iters, tflops, sclk_ghz);
+}
+
 int compass_pick_strategy(const compass_workload *w, const compass_topology *t, const compass_calib *cal,
                           compass_choice *out) {
     return pick(w, t, cal, out);

@@ -28,5 +28,6 @@ int op_sync();
 int op_set_option(int key, long long value);
 int op_kernel_times(double *us, int cap);
 int op_tile_trace(uint32_t *out, int cap);
+int op_probe_mfma(int iters, double *tflops, double *sclk_ghz);
 
 }  // namespace compass

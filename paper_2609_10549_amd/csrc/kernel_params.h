@@ -5,6 +5,7 @@
 namespace compass {
 
 constexpr int kThreads = 256;        // 4 waves of 64, 2 x 2 over the tile
+constexpr int kProbeThreads = 512;   // matrix-core probe: 8 waves per workgroup
 constexpr int kMaxRowTiles = 512;    // row tiles per launch
 constexpr int kMaxParts = 64;        // partitions per launch (2 n, n <= 32)
 constexpr int kMaxFlags = 2048;      // arrival / done flag slots

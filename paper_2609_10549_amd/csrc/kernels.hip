@@ -643,6 +643,56 @@ __global__ __launch_bounds__(64) void join_kernel(const JoinParams j) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
 }
 
+// Matrix-core probe: every wave issues `iters` rounds of 8 independent
+// v_mfma_f32_32x32x16_bf16 and reads the shader-clock counter (s_memtime)
+// and the 100 MHz real-time counter before and after them; out[3 w ..] gets
+// wave w's two deltas and a value that keeps the products live. The 96 KiB
+// LDS reservation leaves room for one workgroup (8 waves, two per SIMD) per
+// CU, so a grid of one workgroup per CU runs all waves at once.
+__global__ __launch_bounds__(kProbeThreads) void mfma_probe_kernel(uint64_t *out, int iters) {
+    __shared__ float reserve[24 * 1024];
+    const int tid = threadIdx.x;
+    bf16x8 a, b;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        a[i] = (__bf16)(0.001f * (float)((tid + i) & 15));
+        b[i] = (__bf16)(0.002f * (float)(i + 1));
+    }
+    f32x16 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
+    const uint64_t t0 = __builtin_amdgcn_s_memtime();
+    const uint64_t r0 = __builtin_amdgcn_s_memrealtime();
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[j], 0, 0, 0);
+    }
+    const uint64_t t1 = __builtin_amdgcn_s_memtime();
+    const uint64_t r1 = __builtin_amdgcn_s_memrealtime();
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sum += acc[j][e];
+    // one exchange through the reservation keeps it allocated
+    reserve[tid] = sum;
+    __syncthreads();
+    const float other = reserve[tid ^ 64];
+    const size_t w = (size_t)blockIdx.x * (kProbeThreads / 64) + (tid >> 6);
+    if ((tid & 63) == 0) {
+        out[3 * w + 0] = t1 - t0;
+        out[3 * w + 1] = r1 - r0;
+        out[3 * w + 2] = (uint64_t)__builtin_bit_cast(uint32_t, sum + other);
+    }
+}
+
+hipError_t launch_mfma_probe(uint64_t *out, int grid, int iters, hipStream_t stream) {
+    hipLaunchKernelGGL(mfma_probe_kernel, dim3(grid), dim3(kProbeThreads), 0, stream, out, iters);
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmParams &p, int cfg, bool rs, hipStream_t stream) {
     if (cfg == kTile256) {
         if (rs) hipLaunchKernelGGL((gemm_kernel<256, 256, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);

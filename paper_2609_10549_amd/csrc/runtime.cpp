@@ -50,6 +50,7 @@ namespace compass {
 
 hipError_t launch_gemm(const GemmParams &p, int cfg, bool rs, hipStream_t stream);
 hipError_t launch_join(const JoinParams &j, hipStream_t stream);
+hipError_t launch_mfma_probe(uint64_t *out, int grid, int iters, hipStream_t stream);
 
 // ---------------------------------------------------------------- errors
 static thread_local std::string t_err;
@@ -132,6 +133,7 @@ struct Ctx {
     bool ready = false;
     int device = -1;
     int num_cu = 0;
+    uint64_t *probe_out = nullptr;   // matrix-core probe results (3 words per wave)
     hsa_agent_t gpu{}, cpu{};
     std::vector<uint32_t> engines;   // SDMA engines usable device->device
     uint32_t *ctrl = nullptr;        // device memory
@@ -1078,6 +1080,43 @@ static int begin(void) {
     int rc = ensure_init();
     if (rc != COMPASS_OK) return rc;
     return take_async_error();
+}
+
+int op_probe_mfma(int iters, double *tflops, double *sclk_ghz) {
+    if (iters < 1 || iters > (1 << 22)) return set_error(COMPASS_ERR_INVALID, "iters out of range [1, 2^22]");
+    if (!tflops || !sclk_ghz) return set_error(COMPASS_ERR_INVALID, "null output pointer");
+    int rc = begin();
+    if (rc != COMPASS_OK) return rc;
+    Ctx &c = g_ctx;
+    const int grid = c.num_cu;
+    const size_t waves = (size_t)grid * (kProbeThreads / 64);
+    hipError_t e = hipSuccess;
+    if (!c.probe_out) e = hipMalloc((void **)&c.probe_out, waves * 3 * sizeof(uint64_t));
+    if (e != hipSuccess) return hip_fail(e, "probe buffer");
+    hipEvent_t a = nullptr, b = nullptr;
+    e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    if (e == hipSuccess) e = hipEventRecord(a, nullptr);
+    if (e == hipSuccess) e = launch_mfma_probe(c.probe_out, grid, iters, nullptr);
+    if (e == hipSuccess) e = hipEventRecord(b, nullptr);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+    std::vector<uint64_t> h(waves * 3);
+    if (e == hipSuccess) e = hipMemcpy(h.data(), c.probe_out, h.size() * sizeof(uint64_t), hipMemcpyDeviceToHost);
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    if (e != hipSuccess) return hip_fail(e, "matrix-core probe");
+    double cyc = 0.0, rt = 0.0;
+    for (size_t w = 0; w < waves; ++w) {
+        cyc += (double)h[3 * w];
+        rt += (double)h[3 * w + 1];
+    }
+    if (!(rt > 0.0) || !(ms > 0.f)) return set_error(COMPASS_ERR_HIP, "matrix-core probe recorded no time");
+    const double flops = 2.0 * 32 * 32 * 16 * 8.0 * (double)iters * (double)waves;
+    *tflops = flops / ((double)ms * 1e-3) / 1e12;
+    *sclk_ghz = cyc / rt * 0.1;   // real-time counter ticks at 100 MHz
+    return COMPASS_OK;
 }
 
 // ---------------------------------------------------------------- operators

@@ -3,12 +3,19 @@
     python -m paper_2609_10549_amd.profile_summary trace <kernel_trace.csv> <last_n> <out.md> <command...>
     python -m paper_2609_10549_amd.profile_summary traffic <fetch_dir> <write_dir> <copy_fetch_dir> \
         <copy_write_dir> <kernel substring> <out.json> [command that made each dir ...]
+    python -m paper_2609_10549_amd.profile_summary mfma <counter_dir> <copy_trace_dir> <last_n> <out.md> \
+        <command...>
 
 `trace` averages the last `last_n` dispatches of every kernel (the timed
 steps of `bench.py --profile-only`). `traffic` converts the FETCH_SIZE and
 WRITE_SIZE counters (KiB per dispatch) of one kernel into bytes per launch,
 each scaled by what the same counter reads for a plain 256 MiB copy kernel,
-and records a hash of the kernel source the counters were taken with."""
+and records a hash of the kernel source the counters were taken with. `mfma`
+reports MfmaUtil (matrix-core busy cycles over active cycles of every SIMD)
+and the bf16 MFMA work of every GEMM kernel, averaged over its last `last_n`
+dispatches, and the SDMA side from a memory-copy trace: device-to-device
+copies grouped into transfer jobs (gaps above 30 us split them), each copy
+2 MiB (the unpaced slice size every benchmark copy uses)."""
 from __future__ import annotations
 
 import csv
@@ -74,8 +81,64 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, kernel_sub, out, *comm
     print(json.dumps(rec))
 
 
+SLICE_BYTES = 2 << 20
+
+
+def mfma(counter_dir, copy_dir, last_n, out, command):
+    by = defaultdict(lambda: defaultdict(list))
+    for path in glob.glob(os.path.join(counter_dir, "*counter_collection.csv")):
+        for r in csv.DictReader(open(path)):
+            by[r["Kernel_Name"].split("(")[0].replace("void ", "")][r["Counter_Name"]].append(
+                (int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+    lines = ["# Matrix-core utilisation and SDMA copy rates, bench.py --profile-only", "",
+             f"Command: `{command}`", "",
+             f"GEMM kernels, last {last_n} dispatches each (MfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs / "
+             "(GRBM_GUI_ACTIVE x SIMDs)):", "",
+             "| kernel | dispatches | MfmaUtil % | bf16 MFMA GFLOP per dispatch |", "|---|---|---|---|"]
+    for name, d in sorted(by.items()):
+        if "gemm_kernel" not in name:
+            continue
+        util = [v for _, v in sorted(d["MfmaUtil"])][-last_n:]
+        mops = [v for _, v in sorted(d["SQ_INSTS_VALU_MFMA_MOPS_BF16"])][-last_n:]
+        lines.append(f"| `{name}` | {len(util)} | {sum(util) / len(util):.1f} | "
+                     f"{sum(mops) / len(mops) * 512 / 1e9:.1f} |")
+    copies = []
+    for path in glob.glob(os.path.join(copy_dir, "*memory_copy_trace.csv")):
+        for r in csv.DictReader(open(path)):
+            if r["Direction"].endswith("DEVICE_TO_DEVICE"):
+                copies.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    copies.sort()
+    jobs, cur = [], []
+    for c in copies:
+        if cur and c[0] - max(e for _, e in cur) > 30_000:
+            jobs.append(cur)
+            cur = []
+        cur.append(c)
+    if cur:
+        jobs.append(cur)
+    tail = jobs[-last_n:]
+    dur = sorted((e - b) / 1e3 for j in tail for b, e in j)
+    pct = lambda q: dur[min(len(dur) - 1, int(q * len(dur)))]  # noqa: E731
+    lines += ["", f"SDMA device-to-device copies: {len(copies)} in {len(jobs)} transfer jobs; the last {len(tail)} "
+              "jobs:", "",
+              f"* per copy (2 MiB): duration p10 / p50 / p90 = {pct(0.1):.1f} / {pct(0.5):.1f} / {pct(0.9):.1f} us, "
+              f"i.e. {SLICE_BYTES / pct(0.5) / 1e3:.1f} GB/s per copy at the median",
+              "", "The memory-copy tracer intercepts every copy call on the host, which stretches a job's "
+              "span against an untraced run (the benchmark's own transfer-alone times are the reference); the "
+              "per-copy durations are the engines' own.", "",
+              "| job | copies | span us | aggregate GB/s |", "|---|---|---|---|"]
+    for i, j in enumerate(tail):
+        span = (max(e for _, e in j) - min(b for b, _ in j)) / 1e3
+        lines.append(f"| {i} | {len(j)} | {span:.1f} | {len(j) * SLICE_BYTES / span / 1e3:.1f} |")
+    lines += ["", f"Kernel source hash: {kernel_source_hash()}"]
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "trace":
         trace(sys.argv[2], int(sys.argv[3]), sys.argv[4], " ".join(sys.argv[5:]))
+    elif sys.argv[1] == "mfma":
+        mfma(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], " ".join(sys.argv[6:]))
     else:
         traffic(*sys.argv[2:])

@@ -397,6 +397,18 @@ def test_kernel_times_one_per_launch():
         C.compass_set_option(C.OPT_KERNEL_TIMING, 0)
 
 
+# ------------------------------------------------------------ matrix-core probe
+def test_probe_mfma_reports_a_plausible_rate_and_clock():
+    _say("matrix-core probe")
+    with pytest.raises(C.CompassError):
+        C.compass_probe_mfma(0)
+    C.compass_probe_mfma(256)
+    tf, ghz = C.compass_probe_mfma(8192)
+    # bounded by the nominal bf16 peak at the maximum clock (2.4 GHz)
+    assert 100.0 < tf < 2516.6 * 1.02, tf
+    assert 0.5 < ghz < 2.5, ghz
+
+
 # ------------------------------------------------------------ paced links and the tile trace
 def test_paced_link_never_beats_its_rate():
     # 7 items of 512 KiB per ring direction at 20 GB/s: the last flag is due
@@ -409,17 +421,21 @@ def test_paced_link_never_beats_its_rate():
     lk = C.links(rate, rate)
     C.compass_transfer(case.problem, lk)   # warm
     C.compass_sync()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    C.compass_transfer(case.problem, lk)
-    b.record()
-    b.synchronize()
-    C.compass_sync()
-    t = a.elapsed_time(b) * 1e-3
     per_ring = (n - 1) * (M // (2 * n)) * K * 2
-    _say("paced transfer", t, per_ring / rate)
-    assert t >= 0.98 * per_ring / rate
-    assert t < 3.0 * per_ring / rate + 2e-3
+    times = []
+    for _ in range(3):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        C.compass_transfer(case.problem, lk)
+        b.record()
+        b.synchronize()
+        C.compass_sync()
+        times.append(a.elapsed_time(b) * 1e-3)
+    _say("paced transfer", times, per_ring / rate)
+    assert min(times) >= 0.98 * per_ring / rate      # no call beats the rate
+    # and pacing is not grossly slow (the best of three, so that one late
+    # wake-up of the host pacer thread does not decide)
+    assert min(times) < 3.0 * per_ring / rate + 2e-3
     assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
 
 
