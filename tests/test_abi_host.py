@@ -157,3 +157,72 @@ def test_calibrate_keeps_fields_without_data():
                           alpha_fusion=5.0, beta_fusion=6.0, d_max=16)
     C.compass_calibrate([], cal)
     assert (cal.comp_a, cal.beta_fusion) == (1.0, 6.0)
+
+
+# ------------------------------------------------------------ argument validation (host only)
+def _fake_problem(pattern, M, N, K, n, rank=0, ring=C.RING_SINGLE):
+    """A problem whose buffers are placeholder addresses: every call below
+    must be refused by the host-side checks, before anything is enqueued."""
+    fake = 0x100000
+    srcs = (ctypes.c_void_p * max(n, 1))(*([fake] * max(n, 1)))
+    st = C.compass_problem(pattern=pattern, M=M, N=N, K=K, n=n, rank=rank, ring=ring, W=fake, C=fake,
+                           shard_src=srcs, gathered=fake, A=fake, partial_src=srcs, partial_stage=fake,
+                           send_dst=None)
+    return st, srcs
+
+
+@pytest.mark.parametrize("pattern", [C.AG_GEMM, C.GEMM_RS])
+def test_degenerate_and_oversized_problems_are_refused_before_enqueue(pattern):
+    lib = C.lib()
+    lk = C.links(0.0, 0.0)
+    call = lib.compass_ag_gemm if pattern == C.AG_GEMM else lib.compass_gemm_rs
+    cases = [
+        ((0, 64, 64, 2), C.ERR_INVALID),          # empty M
+        ((64, 0, 64, 2), C.ERR_INVALID),          # empty N
+        ((64, 64, 0, 2), C.ERR_INVALID),          # empty K
+        ((66, 64, 64, 4), C.ERR_INVALID),         # M not divisible by the partition count
+        ((64, 60, 64, 2), C.ERR_INVALID),         # N not a multiple of 8
+        ((64, 64, 60, 2), C.ERR_INVALID),         # K not a multiple of 8
+        ((64, 64, 64, 0), C.ERR_INVALID),         # no ranks
+        ((128, 64, 64, 33), C.ERR_INVALID),       # more ranks than the flag masks hold
+        ((65536, 64, 8200, 2), C.ERR_UNSUPPORTED),   # A above 1 GiB
+        ((64, 65536, 8200, 2), C.ERR_UNSUPPORTED),   # W above 1 GiB
+    ]
+    for (M, N, K, n), want in cases:
+        st, keep = _fake_problem(pattern, M, N, K, n)
+        assert call(ctypes.byref(st), ctypes.byref(lk), None) == want, (M, N, K, n)
+        assert lib.compass_decomp_gemm(ctypes.byref(st), 1, ctypes.byref(lk), None) == want, (M, N, K, n)
+    # rank out of range, unknown ring, missing buffers, bad links
+    st, keep = _fake_problem(pattern, 64, 64, 64, 2, rank=2)
+    assert call(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+    st, keep = _fake_problem(pattern, 64, 64, 64, 2, ring=7)
+    assert call(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+    st, keep = _fake_problem(pattern, 64, 64, 64, 2)
+    st.W = None
+    assert call(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+    st, keep = _fake_problem(pattern, 64, 64, 64, 2)
+    for bad in (C.links(5e7, 5e7), C.links(float("nan")), C.links(0.0, 0.0, slice_bytes=1024),
+                C.links(0.0, 0.0, engines_per_ring=-1)):
+        assert call(ctypes.byref(st), ctypes.byref(bad), None) == C.ERR_INVALID
+    assert call(None, ctypes.byref(lk), None) == C.ERR_INVALID
+    assert call(ctypes.byref(st), None, None) == C.ERR_INVALID
+    # InterDecom degree: a power of two dividing the rows of a partition
+    st, keep = _fake_problem(pattern, 64, 64, 64, 2)
+    for d in (0, 3, 64):
+        assert lib.compass_decomp_gemm(ctypes.byref(st), d, ctypes.byref(lk), None) == C.ERR_INVALID
+    # the wrong entry point for the pattern
+    other = lib.compass_gemm_rs if pattern == C.AG_GEMM else lib.compass_ag_gemm
+    assert other(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+    assert "" != C.lib().compass_last_error().decode()
+
+
+def test_plain_gemm_refuses_degenerate_shapes():
+    lib = C.lib()
+    fake = ctypes.c_void_p(0x100000)
+    for M, N, K in ((0, 8, 8), (8, 0, 8), (8, 8, 0), (8, 12, 8), (8, 8, 12)):
+        assert lib.compass_gemm(M, N, K, fake, fake, fake, None, None) == C.ERR_INVALID
+    assert lib.compass_gemm(8, 8, 8, None, fake, fake, None, None) == C.ERR_INVALID
+    assert lib.compass_gemm(65536, 64, 8200, fake, fake, fake, None, None) == C.ERR_UNSUPPORTED
+    for it in (0, -1, 1 << 23):
+        a, b = ctypes.c_double(), ctypes.c_double()
+        assert lib.compass_probe_mfma(it, ctypes.byref(a), ctypes.byref(b)) == C.ERR_INVALID

@@ -125,7 +125,7 @@ def test_decomp_d16_split_integer_exact():
 
 # ------------------------------------------------------------ fused AllGather+GEMM
 @pytest.mark.parametrize("ring", ["single", "double"])
-@pytest.mark.parametrize("n", [2, 4, 8])
+@pytest.mark.parametrize("n", [1, 2, 4, 8, 32])   # 1: nothing to gather; 32 double: 64 partitions, the most
 def test_ag_gemm_integer_exact_all_ranks(ring, n):
     M, N, K = 64 * n * (2 if ring == "double" else 1) + 0, 264, 200
     inp = make_int_ag_inputs(M, N, K, n, seed=10 + n)
@@ -187,7 +187,7 @@ def test_ag_gemm_nan_poison():
 
 # ------------------------------------------------------------ fused GEMM+ReduceScatter
 @pytest.mark.parametrize("ring", ["single", "double"])
-@pytest.mark.parametrize("n", [2, 4, 8])
+@pytest.mark.parametrize("n", [1, 2, 4, 8, 32])   # 32 double: a 128-row tile spans 2 of 64 partitions
 def test_gemm_rs_integer_exact(ring, n):
     M, N, K = 128 * n, 264, 136
     inp = make_int_rs_inputs(M, N, K, n, seed=20 + n)
