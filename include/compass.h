@@ -212,7 +212,8 @@ int compass_sync(void);
                                        traffic; 0 = every engine that accepts a copy */
 #define COMPASS_OPT_KERNEL_TIMING 7 /* 1: record HIP events on the launch stream around
                                        every GEMM kernel (up to 512 between reads) */
-#define COMPASS_OPT_TILE_TRACE   8  /* > 0: record one timing record per output tile of
+#define COMPASS_OPT_TILE_TRACE   8  /* > 0: record one timing record per work item (an
+                                       output tile, or one K slice of a split tile) of
                                        every GEMM launch, up to this many records
                                        (a device buffer of value * 32 bytes); 0 = off */
 #define COMPASS_OPT_SCHED        9  /* work dealing, bit mask (default 7): 1 = gated
@@ -235,9 +236,10 @@ int compass_kernel_times(double *us, int cap);
  * the overlap analysis; needs COMPASS_OPT_TILE_TRACE > 0). Synchronizes the
  * device, copies at most `cap` records of 8 uint32 each into host memory
  * `records` (caller-owned, 32 * cap bytes) and returns the number copied, or
- * a negative status. Records are in launch order, one block of
- * tiles_m * tiles_n records per launch, indexed by the tile's position in the
- * launch's ready order: [0] position, [1] row tile << 16 | column tile,
+ * a negative status. Records are in launch order, one block per launch with
+ * one record per work item (a tile, or one K slice of a split tile), indexed
+ * by the item's position in the launch's ready order: [0] position, [1] row
+ * tile << 16 | column tile,
  * [2] HW_ID and [3] XCC_ID of the workgroup that ran it, [4..7] the GPU's
  * 100 MHz real-time counter (low 32 bits) when the workgroup took the ticket,
  * passed the arrival gate (ReduceScatter: the epilogue's gate, so [5] comes

@@ -516,23 +516,54 @@ void gemm_kernel(const GemmParams p) {
         if (finish) {
             if (p.ksplit > 1) {
                 const float *ws0 = p.split_ws + (size_t)tpos * p.ksplit * (BM * BN);
-                for (int e = tid; e < BM * BN / 4; e += kThreads) {
-                    const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
-                    // every slice's load in flight at once, then the sum in slice order
-                    f32x4 part[kMaxSplit];
+                // B elements of 4 per thread at a time, all their slices' loads
+                // (and the partial sum's) in flight at once, then each summed in
+                // slice order: the workspace is uncached, so every load costs a
+                // memory round trip, and B of them overlap
+                auto finish_split = [&](auto b_const, auto s_const) {
+                    constexpr int B = decltype(b_const)::value, S = decltype(s_const)::value;
+                    constexpr int E = BM * BN / 4;
+                    static_assert(E % (kThreads * B) == 0, "whole batches");
+                    for (int e0 = tid; e0 < E; e0 += kThreads * B) {
+                        f32x4 part[B][S];
+                        f32x4 pv[B];
 #pragma unroll
-                    for (int jj = 0; jj < kMaxSplit; ++jj)
-                        if (jj < p.ksplit)
-                            part[jj] = *reinterpret_cast<const f32x4 *>(ws0 + (size_t)jj * (BM * BN) + row * BN + col);
-                    f32x4 sum = part[0];
+                        for (int b = 0; b < B; ++b) {
+                            const int e = e0 + b * kThreads;
+                            const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
 #pragma unroll
-                    for (int jj = 1; jj < kMaxSplit; ++jj)
-                        if (jj < p.ksplit) {
-                            sum[0] += part[jj][0]; sum[1] += part[jj][1];
-                            sum[2] += part[jj][2]; sum[3] += part[jj][3];
+                            for (int jj = 0; jj < S; ++jj)
+                                if (jj < p.ksplit)
+                                    part[b][jj] = *reinterpret_cast<const f32x4 *>(ws0 + (size_t)jj * (BM * BN) +
+                                                                                    row * BN + col);
+                            pv[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                            const int m = m0 + row, n = n0 + col;
+                            if (has_p && m < p.M && n < p.N)
+                                pv[b] = *reinterpret_cast<const f32x4 *>(p.P + (size_t)map_row(p, m) * p.ldp + n);
                         }
-                    store4(row, col, sum[0], sum[1], sum[2], sum[3], has_p);
-                }
+#pragma unroll
+                        for (int b = 0; b < B; ++b) {
+                            const int e = e0 + b * kThreads;
+                            const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
+                            f32x4 sum = part[b][0];
+#pragma unroll
+                            for (int jj = 1; jj < S; ++jj)
+                                if (jj < p.ksplit) {
+                                    sum[0] += part[b][jj][0]; sum[1] += part[b][jj][1];
+                                    sum[2] += part[b][jj][2]; sum[3] += part[b][jj][3];
+                                }
+                            store4(row, col, sum[0] + pv[b][0], sum[1] + pv[b][1], sum[2] + pv[b][2],
+                                   sum[3] + pv[b][3], false);
+                        }
+                    }
+                };
+                // (half the batch in the ReduceScatter variant, whose partial-sum
+                // epilogue leaves fewer registers)
+                constexpr int BB = RS ? 2 : 4;
+                if (p.ksplit <= 8)
+                    finish_split(std::integral_constant<int, BB>{}, std::integral_constant<int, 8>{});
+                else
+                    finish_split(std::integral_constant<int, BB / 2>{}, std::integral_constant<int, kMaxSplit>{});
             } else if (has_p) {
                 // as through_patch, with each 32 x 32 block's fp32 partial
                 // brought into LDS by buffer_load ... lds one block ahead of
