@@ -112,6 +112,8 @@ def summarize(points: list) -> dict:
         aw = [abs(p["model_aware"][str(d)] - p["t_decomp"][str(d)]) for p in points if str(d) in p["t_decomp"]]
         ag = [abs(p["model_agnostic"][str(d)] - p["t_decomp"][str(d)]) for p in points if str(d) in p["t_decomp"]]
         tm = [p["t_decomp"][str(d)] for p in points if str(d) in p["t_decomp"]]
+        if not tm:
+            continue
         mae[str(d)] = dict(aware_us=1e6 * float(np.mean(aw)), agnostic_us=1e6 * float(np.mean(ag)),
                            mean_time_us=1e6 * float(np.mean(tm)), cases=len(aw))
     all_aw = [abs(p["model_aware"][k] - p["t_decomp"][k]) for p in points for k in p["t_decomp"] if k != "1"]
