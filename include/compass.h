@@ -59,6 +59,17 @@ extern "C" {
 #define COMPASS_RING_DOUBLE 1  /* two counter-rotating rings, each chunk split
                                   into a forward and a backward half
                                   (Section III-A, Fig. 5(b); III-B, Fig. 6) */
+#define COMPASS_RING_DOUBLE_SPLIT 2  /* not the paper's design, an extension of it
+                                  for unequal directions: the double ring with
+                                  each chunk's rows split in proportion to the
+                                  two link rates (backward share first, rounded
+                                  to 8 rows, at least 8 rows each way), so that
+                                  both directions finish every step together;
+                                  the schedule is COMPASS_RING_DOUBLE's. With a
+                                  rate <= 0 (unpaced) the split is in halves.
+                                  InterDecom sub-operators split each piece
+                                  the same way. Model: a step carries m/n over
+                                  both rings at B_fwd + B_bwd. */
 
 #define COMPASS_INTRA_FUSION 0  /* TA-IntraFusion  (Algorithm 1) */
 #define COMPASS_INTER_DECOM  1  /* ODP-InterDecom  (Algorithm 1) */

@@ -28,8 +28,10 @@ Contents
     selection), Algorithm 1, and the calibration fits (Section IV-C,
     Section V)
 
-Readings of points the paper leaves open are listed in the design doc of the
-repository; each function states the reading it takes.
+Where the paper leaves a point open, the function states the reading it
+takes. ``DOUBLE_SPLIT`` (a double ring whose chunk rows are split between
+the directions in proportion to their rates) is not the paper's design,
+which splits every chunk in halves; it is an extension of it.
 
 Parity status
   * GEMM parts, schedules, ring bandwidths, Eq. 2-8 identities: pinned by
@@ -50,6 +52,7 @@ AG = "ag"
 RS = "rs"
 SINGLE = "single"
 DOUBLE = "double"
+DOUBLE_SPLIT = "double_split"   # double ring, chunk rows split in proportion to the two rates
 
 # --------------------------------------------------------------------------
 # bf16 <-> fp64
@@ -204,7 +207,7 @@ def schedule(pattern: str, ring: str, n: int, r: int) -> list:
         # step s: the chunk that has travelled s hops on the forward ring
         for s in range(n):
             out.append((r - s) % n)
-    elif pattern == AG and ring == DOUBLE:
+    elif pattern == AG and ring in (DOUBLE, DOUBLE_SPLIT):
         out += [2 * r, 2 * r + 1]            # local data first
         for s in range(1, n):
             out.append(2 * ((r - s) % n) + 1)   # odd, forward ring, from r-1
@@ -212,7 +215,7 @@ def schedule(pattern: str, ring: str, n: int, r: int) -> list:
     elif pattern == RS and ring == SINGLE:
         for s in range(n):
             out.append((r - 1 - s) % n)         # local chunk r comes last
-    elif pattern == RS and ring == DOUBLE:
+    elif pattern == RS and ring in (DOUBLE, DOUBLE_SPLIT):
         for s in range(n):
             out.append(2 * ((r - 1 - s) % n) + 1)
             out.append(2 * ((r + 1 + s) % n))
@@ -355,6 +358,13 @@ def t_comm(pattern: str, ring: str, M: int, N: int, K: int, n: int,
     slowest active ring sets the pace (Section III-A). A per-step latency tau
     is added. Under ReduceScatter, the incoming and outgoing halves of a step
     use the two directions of the link and overlap."""
+    if ring == DOUBLE_SPLIT:
+        # each step's chunk (m/n) is split between the rings in proportion to
+        # their rates, so both rings finish the step together
+        c_in, c_out = comm_bytes_per_step(pattern, SINGLE, M, N, K, n, a_bytes, p_bytes, o_bytes)
+        f_bwd = bwd_Bps / (fwd_Bps + bwd_Bps)
+        step = max(max(x * (1.0 - f_bwd) / fwd_Bps, x * f_bwd / bwd_Bps) for x in (c_in, c_out))
+        return (n - 1) * (step + tau)
     b_in, b_out = comm_bytes_per_step(pattern, ring, M, N, K, n, a_bytes, p_bytes, o_bytes)
     rates = [fwd_Bps] if ring == SINGLE else [fwd_Bps, bwd_Bps]
     step = max(max(b_in / r, b_out / r) for r in rates)

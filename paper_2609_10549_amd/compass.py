@@ -38,7 +38,8 @@ OPT_TILE_TRACE = 8
 OPT_SCHED = 9
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
-RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE}
+RING_DOUBLE_SPLIT = 2
+RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE, "double_split": RING_DOUBLE_SPLIT}
 
 
 class CompassError(RuntimeError):

@@ -16,7 +16,7 @@ int schedule_fill(int pattern, int ring, int n, int rank, int32_t *out, int cap)
         return set_error(COMPASS_ERR_INVALID, "schedule: need 1 <= n <= 32 and 0 <= rank < n");
     if (pattern != COMPASS_AG_GEMM && pattern != COMPASS_GEMM_RS)
         return set_error(COMPASS_ERR_INVALID, "schedule: unknown pattern");
-    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE)
+    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE && ring != COMPASS_RING_DOUBLE_SPLIT)
         return set_error(COMPASS_ERR_INVALID, "schedule: unknown ring");
     const int len = ring == COMPASS_RING_SINGLE ? n : 2 * n;
     if (!out || cap < len) return set_error(COMPASS_ERR_INVALID, "schedule: output too small");
@@ -64,6 +64,12 @@ static void step_bytes(const compass_workload &w, int ring, double *in, double *
 
 double model_t_comm(const compass_workload &w, const compass_topology &t) {
     double in, out;
+    if (t.ring == COMPASS_RING_DOUBLE_SPLIT) {
+        // the step's whole chunk over both rings, each carrying its rate's share
+        step_bytes(w, COMPASS_RING_SINGLE, &in, &out);
+        const double both = t.fwd_Bps + t.bwd_Bps;
+        return (w.n - 1) * (std::fmax(in, out) / both + t.step_latency_s);
+    }
     step_bytes(w, t.ring, &in, &out);
     double step = 0.0;
     const int rings = t.ring == COMPASS_RING_SINGLE ? 1 : 2;
@@ -123,9 +129,9 @@ int pick(const compass_workload *w, const compass_topology *t, const compass_cal
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: bad workload");
     if (w->pattern != COMPASS_AG_GEMM && w->pattern != COMPASS_GEMM_RS)
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown pattern");
-    if (t->ring != COMPASS_RING_SINGLE && t->ring != COMPASS_RING_DOUBLE)
+    if (t->ring != COMPASS_RING_SINGLE && t->ring != COMPASS_RING_DOUBLE && t->ring != COMPASS_RING_DOUBLE_SPLIT)
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown ring");
-    if (!(t->fwd_Bps > 0) || (t->ring == COMPASS_RING_DOUBLE && !(t->bwd_Bps > 0)))
+    if (!(t->fwd_Bps > 0) || (t->ring != COMPASS_RING_SINGLE && !(t->bwd_Bps > 0)))
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: link rates must be positive");
     if (cal->d_max < 1) return set_error(COMPASS_ERR_INVALID, "pick_strategy: d_max < 1");
     // Phase 1: base metrics

@@ -653,17 +653,45 @@ static std::vector<uint32_t> engines_for(int role, const std::vector<int> &activ
 struct Geometry {
     int P;           // partitions
     int rows;        // rows per chunk
-    int prow;        // rows per partition
+    int prow;        // rows per partition (double ring: half a chunk)
+    bool dbl;        // double ring (either split)
+    double fb;       // double ring: share of a chunk's rows on the backward ring
     int32_t sched[2 * kMaxRanks];
     int pos[2 * kMaxRanks];   // position of each partition in the schedule
 };
+
+// Rows of the backward (first) part of a block of r rows of one chunk under
+// the double ring: half of it, or (proportional split) the backward ring's
+// share of the two rates, rounded to 8 rows and leaving at least 8 (or half
+// the block, if smaller) to each ring.
+static int half0(const Geometry &g, int r) {
+    if (g.fb == 0.5) return r / 2;
+    const int lo = std::min(8, r / 2);
+    const int h = (int)std::llround(r * g.fb / 8.0) * 8;
+    return std::min(std::max(h, lo), r - lo);
+}
+
+// Partition holding global row r (the fused operators' arrival gates).
+static int part_of_row(const Geometry &g, int r) {
+    const int c = r / g.rows;
+    if (!g.dbl) return c;
+    return 2 * c + ((r - c * g.rows) < half0(g, g.rows) ? 0 : 1);
+}
+
+// Rows of the smallest partition.
+static int min_part_rows(const Geometry &g) {
+    if (!g.dbl) return g.rows;
+    const int h0 = half0(g, g.rows);
+    return std::min(h0, g.rows - h0);
+}
 
 static int validate(const compass_problem *p, const compass_links *l, int want_pattern, Geometry *g) {
     if (!p) return set_error(COMPASS_ERR_INVALID, "problem is NULL");
     if (!l) return set_error(COMPASS_ERR_INVALID, "links is NULL");
     if (want_pattern >= 0 && p->pattern != want_pattern) return set_error(COMPASS_ERR_INVALID, "wrong pattern for this call");
     if (p->pattern != COMPASS_AG_GEMM && p->pattern != COMPASS_GEMM_RS) return set_error(COMPASS_ERR_INVALID, "unknown pattern");
-    if (p->ring != COMPASS_RING_SINGLE && p->ring != COMPASS_RING_DOUBLE) return set_error(COMPASS_ERR_INVALID, "unknown ring");
+    if (p->ring != COMPASS_RING_SINGLE && p->ring != COMPASS_RING_DOUBLE && p->ring != COMPASS_RING_DOUBLE_SPLIT)
+        return set_error(COMPASS_ERR_INVALID, "unknown ring");
     if (p->n < 1 || p->n > kMaxRanks || p->rank < 0 || p->rank >= p->n)
         return set_error(COMPASS_ERR_INVALID, "need 1 <= n <= %d and 0 <= rank < n", kMaxRanks);
     if (p->M < 1 || p->N < 1 || p->K < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
@@ -695,6 +723,10 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     g->P = P;
     g->rows = p->M / p->n;
     g->prow = p->M / P;
+    g->dbl = p->ring != COMPASS_RING_SINGLE;
+    g->fb = 0.5;
+    if (p->ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0)
+        g->fb = l->bwd_Bps / (l->fwd_Bps + l->bwd_Bps);
     const int len = schedule_fill(p->pattern, p->ring, p->n, p->rank, g->sched, 2 * kMaxRanks);
     if (len != P) return len < 0 ? len : set_error(COMPASS_ERR_INVALID, "schedule failed");
     for (int i = 0; i < P; ++i) g->pos[g->sched[i]] = i;
@@ -748,9 +780,13 @@ static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.
 // rate; ReduceScatter incoming gets two thirds of a direction's engines).
 static double lambda_estimate(const compass_problem *p, const Geometry &geo, const compass_links *l) {
     const double flops = 2.0 * p->M * (double)p->N * p->K;
-    const double step = p->pattern == COMPASS_AG_GEMM ? (double)geo.prow * p->K * 2 : (double)geo.prow * p->N * 4;
-    const bool dbl = p->ring == COMPASS_RING_DOUBLE;
+    double step = p->pattern == COMPASS_AG_GEMM ? (double)geo.prow * p->K * 2 : (double)geo.prow * p->N * 4;
+    const bool dbl = p->ring != COMPASS_RING_SINGLE;
     double rate = dbl ? std::fmin(l->fwd_Bps, l->bwd_Bps) : l->fwd_Bps;
+    if (p->ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0) {
+        step *= 2.0;                        // the whole chunk per step ...
+        rate = l->fwd_Bps + l->bwd_Bps;     // ... over both rings at once
+    }
     if (!(rate > 0)) {
         double e = (double)g_ctx.engines.size() / (dbl ? 2.0 : 1.0);
         if (p->pattern == COMPASS_GEMM_RS) e *= 2.0 / 3.0;
@@ -828,7 +864,7 @@ static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M
     std::vector<std::pair<int, int>> key;
     for (int t = 0; t < g.tiles_m; ++t) {
         const int r0 = t * bm, r1 = std::min(M, r0 + bm) - 1;
-        const int p0 = r0 / geo.prow, p1 = r1 / geo.prow;
+        const int p0 = part_of_row(geo, r0), p1 = part_of_row(geo, r1);
         int k = 0;
         for (int q = p0; q <= p1; ++q) k = std::max(k, geo.pos[q]);
         g.rt_lo[t] = (uint8_t)p0;
@@ -865,6 +901,13 @@ static hipError_t copy_if_needed(void *dst, const void *src, size_t bytes, hipSt
 static inline int part_chunk(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE ? q : q / 2; }
 static inline int part_half(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE ? 0 : q % 2; }
 static inline bool part_fwd(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE || (q % 2) == 1; }
+// Rows [*off, *off + *cnt) of a block of r chunk rows that partition half h carries.
+static inline void part_rows(const compass_problem *p, const Geometry &g, int r, int h, int *off, int *cnt) {
+    if (p->ring == COMPASS_RING_SINGLE) { *off = 0; *cnt = r; return; }
+    const int h0 = half0(g, r);
+    *off = h ? h0 : 0;
+    *cnt = h ? r - h0 : h0;
+}
 
 static int make_item(Item *it, void *dst, const void *src, size_t bytes, int flag, int gate) {
     int rc;
@@ -900,14 +943,15 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
     fwd->wait_start = bwd->wait_start = wait_start;
     const size_t K = (size_t)p->K;
     const int pc = geo.rows / d;                                     // chunk rows per sub-operator
-    const int piece = p->ring == COMPASS_RING_SINGLE ? pc : pc / 2;  // rows per item
     for (int j = 0; j < d; ++j) {
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
             const int c = part_chunk(p, q), h = part_half(p, q);
             if (c == p->rank) continue;
             if (q == g_ctx.drop_flag && d == 1) continue;
-            const size_t row_in_chunk = (size_t)j * pc + (size_t)h * piece;
+            int off, piece;                                          // rows of this item
+            part_rows(p, geo, pc, h, &off, &piece);
+            const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
             const int rc = make_item(&it, (char *)p->gathered + row * K * 2,
@@ -928,10 +972,11 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                    uint64_t resident, bool gate_out, bool wait_start, Job jobs[4]) {
     // incoming fp32 partials carry twice the bytes of the outgoing bf16 sums
     std::vector<int> active{0}, weight{2};
-    if (p->ring == COMPASS_RING_DOUBLE) { active.push_back(1); weight.push_back(2); }
+    const bool dbl = p->ring != COMPASS_RING_SINGLE;
+    if (dbl) { active.push_back(1); weight.push_back(2); }
     if (p->send_dst) {
         active.push_back(2); weight.push_back(1);
-        if (p->ring == COMPASS_RING_DOUBLE) { active.push_back(3); weight.push_back(1); }
+        if (dbl) { active.push_back(3); weight.push_back(1); }
     }
     for (int r = 0; r < 4; ++r) {
         fill_job(jobs[r], l, r % 2 == 0, epoch, r, active, weight);
@@ -939,13 +984,14 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
     }
     const size_t N = (size_t)p->N;
     const int pc = geo.rows / d;
-    const int piece = p->ring == COMPASS_RING_SINGLE ? pc : pc / 2;
     for (int j = 0; j < d; ++j) {
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
             if (resident & (1ull << q)) continue;
             const int c = part_chunk(p, q), h = part_half(p, q);
-            const size_t row_in_chunk = (size_t)j * pc + (size_t)h * piece;
+            int off, piece;
+            part_rows(p, geo, pc, h, &off, &piece);
+            const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
             const int rc = make_item(&it, (char *)p->partial_stage + row * N * 4,
@@ -959,7 +1005,9 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
             const int q = geo.sched[s];
             const int c = part_chunk(p, q), h = part_half(p, q);
             if (c == p->rank) continue;
-            const size_t row_in_chunk = (size_t)j * pc + (size_t)h * piece;
+            int off, piece;
+            part_rows(p, geo, pc, h, &off, &piece);
+            const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
             const int rc = make_item(&it, (char *)p->send_dst[c] + row_in_chunk * N * 2,
@@ -997,16 +1045,24 @@ static int stage_local_shard(const compass_problem *p, const Geometry &geo, hipS
     return e == hipSuccess ? COMPASS_OK : hip_fail(e, "local shard copy");
 }
 
-static int stage_resident_partials(const compass_problem *p, const Geometry &geo, uint64_t resident, hipStream_t s) {
+// The partials of the resident partitions, for each of the d sub-operators
+// the rows its piece of the partition covers (rs_jobs moves the others).
+static int stage_resident_partials(const compass_problem *p, const Geometry &geo, uint64_t resident, int d,
+                                   hipStream_t s) {
     const size_t N = (size_t)p->N;
+    const int pc = geo.rows / d;
     for (int q = 0; q < geo.P; ++q) {
         if (!(resident & (1ull << q))) continue;
         const int c = part_chunk(p, q), h = part_half(p, q);
-        const size_t row_in_chunk = (size_t)h * geo.prow;
-        void *dst = (char *)p->partial_stage + ((size_t)c * geo.rows + row_in_chunk) * N * 4;
-        const void *src = (const char *)p->partial_src[c] + row_in_chunk * N * 4;
-        const hipError_t e = copy_if_needed(dst, src, (size_t)geo.prow * N * 4, s);
-        if (e != hipSuccess) return hip_fail(e, "resident partial copy");
+        int off, cnt;
+        part_rows(p, geo, pc, h, &off, &cnt);
+        for (int j = 0; j < d; ++j) {
+            const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
+            void *dst = (char *)p->partial_stage + ((size_t)c * geo.rows + row_in_chunk) * N * 4;
+            const void *src = (const char *)p->partial_src[c] + row_in_chunk * N * 4;
+            const hipError_t e = copy_if_needed(dst, src, (size_t)cnt * N * 4, s);
+            if (e != hipSuccess) return hip_fail(e, "resident partial copy");
+        }
     }
     return COMPASS_OK;
 }
@@ -1132,7 +1188,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true, geo.prow, lambda_estimate(p, geo, l));
+    const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M, true);
     g.gate = kGateMain;
@@ -1154,10 +1210,10 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     const uint64_t res = resident_mask(p, geo);
     Job jobs[4];
     if ((rc = rs_jobs(p, geo, l, epoch, 1, res, true, true, jobs)) != COMPASS_OK) return rc;
-    if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
+    if ((rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true, geo.prow, lambda_estimate(p, geo, l), true);
+    const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l), true);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M, false);
     g.gate = kGateEpilogue;
@@ -1203,7 +1259,7 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
         if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     } else {
         if ((rc = rs_jobs(p, geo, l, epoch, d, res, true, true, rs)) != COMPASS_OK) return rc;
-        if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
+        if ((rc = stage_resident_partials(p, geo, res, d, s)) != COMPASS_OK) return rc;
         if (p->send_dst)
             for (int r = 2; r < 4; ++r)
                 if (rs[r].final_flag >= 0) finals.push_back(rs[r].final_flag);
@@ -1305,7 +1361,7 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
     const uint64_t res = resident_mask(p, geo);
     Job jobs[4];
     if ((rc = rs_jobs(p, geo, l, epoch, 1, res, false, true, jobs)) != COMPASS_OK) return rc;
-    if ((rc = stage_resident_partials(p, geo, res, s)) != COMPASS_OK) return rc;
+    if ((rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
     const int cfg = pick_tile(p->M, p->N, false);

@@ -39,7 +39,7 @@ def test_struct_sizes_match_c_layout():
 
 
 @pytest.mark.parametrize("pattern", ["ag", "rs"])
-@pytest.mark.parametrize("ring", ["single", "double"])
+@pytest.mark.parametrize("ring", ["single", "double", "double_split"])
 def test_schedule_bit_exact_vs_oracle(pattern, ring):
     for n in [1, 2, 3, 4, 5, 8, 16, 32]:
         for r in range(n):
@@ -92,13 +92,13 @@ def test_pick_strategy_matches_oracle_over_table4():
     wl = O.table4_workloads()
     strategies = set()
     for i, (pat, M, N, K, n) in enumerate(wl):
-        ring = "double" if i % 2 else "single"
+        ring = ("single", "double", "double_split")[i % 3]
         fwd = rng.uniform(5e9, 400e9)
         bwd = fwd / rng.choice([1.0, 4.0])
         cal = dict(comp_a=rng.uniform(0, 2e-5), comp_b=1.0 / rng.uniform(3e14, 2e15),
                    alpha_decomp=rng.uniform(0.7, 1.2), beta_decomp=rng.uniform(0.0, 0.15),
                    alpha_fusion=rng.uniform(0, 5e-5), beta_fusion=rng.uniform(0, 1e-13),
-                   d_max=16, literal_eq5=i % 3 == 0)
+                   d_max=16, literal_eq5=i % 4 == 1)
         got, ref = _pick_both(pat, ring, M, N, K, n, fwd, bwd, rng.uniform(0, 2e-5), cal)
         assert got.d_star == ref["d_star"] and got.d_cand == ref["d_cand"]
         assert got.strategy == (C.INTRA_FUSION if ref["strategy"] == "intra_fusion" else C.INTER_DECOM)

@@ -59,10 +59,20 @@ def rs_rows_reference(inp: dict, rows: np.ndarray) -> np.ndarray:
     return O.gemm_rs(O.bf16_to_f64(inp["A"][rows]), O.bf16_to_f64(inp["W"]), [P], 1)
 
 
-def check_ag(case: AGCase, inp: dict, parts: int, seed: int):
+def split_boundary_rows(inp: dict, frac_bwd: float) -> np.ndarray:
+    """The last backward-ring row and the first forward-ring row of every
+    chunk under a rate-proportional split (rounded to 8 rows)."""
+    rows = inp["M"] // inp["n"]
+    h0 = int(round(rows * frac_bwd / 8.0)) * 8
+    return np.array([c * rows + h0 + o for c in range(inp["n"]) for o in (-1, 0)], dtype=np.int64)
+
+
+def check_ag(case: AGCase, inp: dict, parts: int, seed: int, extra_rows=None):
     torch.cuda.synchronize()
     assert np.array_equal(case.gathered.cpu().numpy().view(np.uint16), np.vstack(inp["shards"]))
     rows = sample_rows(inp["M"], parts, seed)
+    if extra_rows is not None:
+        rows = np.unique(np.concatenate([rows, extra_rows]))
     got = device_rows(case.C, rows)
     assert np.isfinite(got).all()
     err = rel_err(got, ag_rows_reference(inp, rows))
@@ -70,9 +80,11 @@ def check_ag(case: AGCase, inp: dict, parts: int, seed: int):
     assert err < TOL
 
 
-def check_rs(case: RSCase, inp: dict, parts: int, seed: int):
+def check_rs(case: RSCase, inp: dict, parts: int, seed: int, extra_rows=None):
     torch.cuda.synchronize()
     rows = sample_rows(inp["M"], parts, seed)
+    if extra_rows is not None:
+        rows = np.unique(np.concatenate([rows, extra_rows]))
     got = device_rows(case.C, rows)
     assert np.isfinite(got).all()
     err = rel_err(got, rs_rows_reference(inp, rows))
@@ -150,3 +162,20 @@ def test_config5_reducescatter_unpaced_takes_256_tiles():
         C.compass_set_option(C.OPT_TILE_TRACE, 0)
     assert len(rec) == (inp["M"] // 256) * (inp["N"] // 256)
     check_rs(case, inp, 2 * inp["n"], seed=503)
+
+
+@pytest.mark.parametrize("pattern", ["ag", "rs"])
+def test_config5_proportional_double_ring_4_to_1_full_size(pattern):
+    # the same workload with each chunk's rows split 1 : 4 between the rings
+    inp = inputs(5, pattern)
+    _say("config 5 split:", pattern)
+    if pattern == "ag":
+        case = AGCase(inp, 0, "double_split")
+        C.compass_ag_gemm(case.problem, LINKS_4_TO_1)
+        C.compass_sync()
+        check_ag(case, inp, 2 * inp["n"], seed=511, extra_rows=split_boundary_rows(inp, 0.2))
+    else:
+        case = RSCase(inp, 0, "double_split")
+        C.compass_gemm_rs(case.problem, LINKS_4_TO_1)
+        C.compass_sync()
+        check_rs(case, inp, 2 * inp["n"], seed=512, extra_rows=split_boundary_rows(inp, 0.2))

@@ -232,15 +232,17 @@ def test_decomp_ag_integer_exact(ring, d):
     assert np.array_equal(host_bits(case.C), ref)
 
 
+@pytest.mark.parametrize("ring", ["single", "double"])
 @pytest.mark.parametrize("d", [1, 2, 4])
-def test_decomp_rs_integer_exact(d):
+def test_decomp_rs_integer_exact(d, ring):
+    # double ring, d > 1: the resident partitions' partials are staged piece by piece
     n = 4
     M, N, K = 1024, 264, 136
     inp = make_int_rs_inputs(M, N, K, n, seed=50 + d)
     ref = O.f64_to_bf16_rne(O.decomp_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
                                         [p.astype(np.float64) for p in inp["P_in"]], n, d))
-    case = RSCase(inp, 0, "single")
-    _say("decomp rs", d)
+    case = RSCase(inp, 0, ring)
+    _say("decomp rs", d, ring)
     C.compass_decomp_gemm(case.problem, d, FAST)
     C.compass_sync()
     got = host_bits(case.C)
@@ -457,3 +459,84 @@ def test_tile_trace_records_every_work_item():
     assert (d < (1 << 31)).all()
     ref = O.ag_gemm([O.bf16_to_f64(inp["shards"][0])], O.bf16_to_f64(inp["W"]))
     assert np.array_equal(host_bits(Cm), O.f64_to_bf16_rne(ref))
+
+
+# ------------------------------------------------------------ double ring split by link rate
+SPLIT_4_TO_1 = C.links(200e9, 50e9)
+
+
+def test_ag_gemm_proportional_double_ring_integer_exact():
+    # 1024 rows per chunk at 4 : 1 -> 208 rows on the backward ring, 816 forward
+    n = 4
+    M, N, K = 4096, 264, 200
+    inp = make_int_ag_inputs(M, N, K, n, seed=81)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    for r in range(n):
+        for lk in (SPLIT_4_TO_1, C.links(0.0, 0.0)):   # unpaced: halves
+            _say("ag split", r, lk.fwd_Bps)
+            case = AGCase(inp, r, "double_split")
+            C.compass_ag_gemm(case.problem, lk)
+            C.compass_sync()
+            assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+            assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_gemm_rs_proportional_double_ring_integer_exact():
+    n = 4
+    M, N, K = 1024, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=82)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    rows = M // n
+    for r in range(n):
+        _say("rs split", r)
+        case = RSCase(inp, r, "double_split")
+        C.compass_gemm_rs(case.problem, SPLIT_4_TO_1)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+        for q in range(n):
+            if q != r:
+                assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
+
+
+@pytest.mark.parametrize("pattern", ["ag", "rs"])
+@pytest.mark.parametrize("d", [1, 2, 4])
+def test_decomp_proportional_double_ring_integer_exact(pattern, d):
+    n = 4
+    if pattern == "ag":
+        inp = make_int_ag_inputs(2048, 136, 200, n, seed=83)
+        ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+        case = AGCase(inp, 1, "double_split")
+    else:
+        inp = make_int_rs_inputs(2048, 136, 136, n, seed=84)
+        ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                          [p.astype(np.float64) for p in inp["P_in"]], n))
+        case = RSCase(inp, 1, "double_split")
+    _say("decomp split", pattern, d)
+    C.compass_decomp_gemm(case.problem, d, SPLIT_4_TO_1)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), ref)
+
+
+def test_proportional_split_shortens_a_4_to_1_transfer():
+    # 7 steps of one 4 MiB chunk: halves wait 7 x 2 MiB on the 50 GB/s ring
+    # (~294 us); the split finishes both rings after 7 x 4 MiB / 250 GB/s (~117 us)
+    n = 8
+    inp = make_ag_inputs(4096, 64, 4096, n, seed=85)
+    t = {}
+    for ring in ("double", "double_split"):
+        case = AGCase(inp, 0, ring)
+        C.compass_transfer(case.problem, SPLIT_4_TO_1)
+        C.compass_sync()
+        times = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            C.compass_transfer(case.problem, SPLIT_4_TO_1)
+            b.record()
+            b.synchronize()
+            C.compass_sync()
+            times.append(a.elapsed_time(b) * 1e-3)
+        t[ring] = min(times)
+    _say("transfer halves / split", t)
+    assert t["double_split"] < 0.75 * t["double"]

@@ -218,3 +218,34 @@ def test_calibration_eta_fit_from_measurements():
             ys.append(O.eta_observed(t, Tc, Tm, d))
     a, b = O.fit_line(xs, ys)
     assert a == pytest.approx(alpha, abs=1e-12) and b == pytest.approx(beta, abs=1e-12)
+
+
+def test_proportional_double_ring_comm_by_hand():
+    # AllGather n = 8, M x K = 8192 x 4096 bf16: a step moves one 8 MiB chunk.
+    # Split 1:4 between a 50 GB/s backward and a 200 GB/s forward ring, both
+    # finish a step after 8 MiB / 250 GB/s; the halved double ring waits for
+    # its 4 MiB on the slow ring.
+    chunk = 8192 * 4096 * 2 / 8
+    got = O.t_comm(O.AG, O.DOUBLE_SPLIT, 8192, 1, 4096, 8, 200e9, 50e9)
+    assert got == pytest.approx(7 * chunk / 250e9, rel=1e-14)
+    assert O.t_comm(O.AG, O.DOUBLE, 8192, 1, 4096, 8, 200e9, 50e9) == pytest.approx(7 * chunk / 2 / 50e9, rel=1e-14)
+    # ReduceScatter: the fp32 partial in (twice the bf16 sum out) sets the step
+    chunk_in = 8192 * 4096 * 4 / 8
+    got = O.t_comm(O.RS, O.DOUBLE_SPLIT, 8192, 4096, 2048, 8, 200e9, 50e9, tau=1e-6)
+    assert got == pytest.approx(7 * (chunk_in / 250e9 + 1e-6), rel=1e-14)
+
+
+def test_proportional_double_ring_reduces_to_halves_at_equal_rates():
+    rng = random.Random(11)
+    for _ in range(50):
+        pat = rng.choice([O.AG, O.RS])
+        n = rng.choice([2, 4, 8, 16])
+        M, N, K = n * 2 * rng.randint(1, 64) * 8, rng.randint(1, 64) * 64, rng.randint(1, 64) * 64
+        B = rng.uniform(1e9, 500e9)
+        a = O.t_comm(pat, O.DOUBLE_SPLIT, M, N, K, n, B, B)
+        b = O.t_comm(pat, O.DOUBLE, M, N, K, n, B, B)
+        assert a == pytest.approx(b, rel=1e-13)
+        # and never slower than halves at unequal rates
+        f = rng.uniform(0.05, 1.0)
+        assert O.t_comm(pat, O.DOUBLE_SPLIT, M, N, K, n, B, B * f) <= \
+            O.t_comm(pat, O.DOUBLE, M, N, K, n, B, B * f) * (1 + 1e-12)
