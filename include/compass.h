@@ -63,8 +63,10 @@ extern "C" {
                                   for unequal directions: the double ring with
                                   each chunk's rows split in proportion to the
                                   two link rates (backward share first, rounded
-                                  to 8 rows, at least 8 rows each way), so that
-                                  both directions finish every step together;
+                                  to a multiple of 128 rows for chunks of at
+                                  least 1024 rows, else of 8, toward the shorter
+                                  step), so that both directions finish every
+                                  step together, nearly;
                                   the schedule is COMPASS_RING_DOUBLE's. With a
                                   rate <= 0 (unpaced) the split is in halves.
                                   InterDecom sub-operators split each piece

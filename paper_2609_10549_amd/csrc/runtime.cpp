@@ -662,13 +662,20 @@ struct Geometry {
 
 // Rows of the backward (first) part of a block of r rows of one chunk under
 // the double ring: half of it, or (proportional split) the backward ring's
-// share of the two rates, rounded to 8 rows and leaving at least 8 (or half
-// the block, if smaller) to each ring.
+// share of the two rates, rounded to a multiple of G rows (G = 128, the
+// smaller tile's height, for blocks of at least 1024 rows, so that no tile
+// spans both parts; else 8), down or up, whichever gives the shorter step,
+// and leaving at least G (or half the block, if smaller) to each ring.
 static int half0(const Geometry &g, int r) {
     if (g.fb == 0.5) return r / 2;
-    const int lo = std::min(8, r / 2);
-    const int h = (int)std::llround(r * g.fb / 8.0) * 8;
-    return std::min(std::max(h, lo), r - lo);
+    const int G = r >= 1024 ? 128 : 8;
+    const int lo = std::min(G, r / 2);
+    auto clampv = [&](int h) { return std::min(std::max(h, lo), r - lo); };
+    const int dn = clampv((int)std::floor(r * g.fb / G) * G);
+    const int up = clampv((int)std::ceil(r * g.fb / G) * G);
+    // step time in units of 1 / (B_fwd + B_bwd): max(h / fb, (r - h) / (1 - fb))
+    auto step = [&](int h) { return std::fmax(h / g.fb, (r - h) / (1.0 - g.fb)); };
+    return step(up) < step(dn) ? up : dn;
 }
 
 // Partition holding global row r (the fused operators' arrival gates).
@@ -1188,7 +1195,10 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
-    const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l));
+    // (rate-proportional parts: a 256-row tile may span both parts of a
+    // chunk and waits for the later one, which an AllGather tolerates)
+    const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 ? geo.rows : min_part_rows(geo),
+                              lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M, true);
     g.gate = kGateMain;

@@ -17,7 +17,8 @@
   largest N (AllGather 8192x16384x4096) and the largest K (ReduceScatter
   8192x4096x16384), as far as the ceiling allows.
 * The GPT-3 175B shapes (8192 tokens, hidden 12288, TP = 8) over a double
-  ring whose directions run at 4 : 1.
+  ring whose directions run at 4 : 1, with chunks split in halves and split
+  in proportion to the rates (fused, unfused, InterDecom d = 2, 4, 8).
 * torch.matmul (hipBLASLt) on every GEMM shape, for context.
 
 Timing only: the inputs are seeded random bf16 on the GPU (parity is the
@@ -135,29 +136,49 @@ def decomp_study(cal, lam, verbose):
 GPT3_SHAPES = {"ag": (8192, 6144, 12288), "rs": (8192, 12288, 6144)}
 
 
-def gpt3_study(pats, verbose):
-    """GPT-3 175B shapes, double ring with the forward direction 4x the backward one."""
+def gpt3_study(pats, verbose, cal=None):
+    """GPT-3 175B shapes over a double ring whose forward direction runs at 4x
+    the backward one: chunks split in halves (the paper's double ring) and
+    split in proportion to the rates; fused, unfused and InterDecom at
+    d = 2, 4, 8, and the selector's pick for each ring."""
+    import types
     res = []
     for pat in pats:
         M, N, K = GPT3_SHAPES[pat]
-        n, ring = 8, "double"
-        buf = CAL.Buffers(pat, M, N, K, n, ring)
+        n = 8
+        buf = CAL.Buffers(pat, M, N, K, n, "double")
         tg = CAL.time_call(lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P), reps=5)
         tm = _matmul_time(buf, reps=5)
-        per_link = CAL.ring_bytes_per_link(pat, M, N, K, n, ring)
+        per_link = CAL.ring_bytes_per_link(pat, M, N, K, n, "double")
         unpaced = C.links(0.0, 0.0)
         cap = per_link / CAL.time_call(lambda: C.compass_transfer(buf.problem, unpaced), reps=3)
-        # the slow direction at the rate that balances the GEMM, capped so the
-        # fast one (4x) stays below the ceiling
+        # the slow direction at the rate that balances the GEMM on halves,
+        # capped so the fast one (4x) stays below the ceiling
         bwd = min(per_link / tg, CEILING_FRACTION * cap / 4.0)
         lk = C.links(4.0 * bwd, bwd)
-        pt = overlap_point(buf, pat, lk, reps=5)
-        pt.update(pattern=pat, M=M, N=N, K=K, fwd_Bps=4.0 * bwd, bwd_Bps=bwd,
-                  gemm_tflops=2.0 * M * N * K / (pt["t_gemm_us"] * 1e-6) / 1e12, torch_matmul_us=tm * 1e6,
-                  fused_tflops=2.0 * M * N * K / (pt["t_fused_us"] * 1e-6) / 1e12)
-        res.append(pt)
-        if verbose:
-            print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in pt.items()}), flush=True)
+        for ring in ("double", "double_split"):
+            if ring == "double":
+                prob = buf.problem
+            elif pat == "ag":
+                prob = C.ag_problem(buf.shards, buf.gathered, buf.W, buf.C, 0, ring)
+            else:
+                prob = C.rs_problem(buf.A, buf.W, buf.partials, buf.stage, buf.C, buf.send, 0, ring)
+            view = types.SimpleNamespace(A=buf.A, W=buf.W, C=buf.C, P=buf.P, problem=prob)
+            pt = overlap_point(view, pat, lk, reps=5)
+            dec = CAL.time_interleaved({d: (lambda d=d: C.compass_decomp_gemm(prob, d, lk)) for d in (2, 4, 8)},
+                                       reps=5)
+            pt.update(pattern=pat, ring=ring, M=M, N=N, K=K, fwd_Bps=4.0 * bwd, bwd_Bps=bwd,
+                      gemm_tflops=2.0 * M * N * K / (pt["t_gemm_us"] * 1e-6) / 1e12, torch_matmul_us=tm * 1e6,
+                      fused_tflops=2.0 * M * N * K / (pt["t_fused_us"] * 1e-6) / 1e12,
+                      t_decomp_us={str(d): t * 1e6 for d, t in dec.items()})
+            if cal is not None:
+                ch = _pick(pat, M, N, K, n, ring, 4.0 * bwd, bwd, cal)
+                pt.update(pick="intra_fusion" if ch.strategy == C.INTRA_FUSION else "inter_decom",
+                          pick_d=ch.d_star, model_t_comm_us=ch.t_comm * 1e6)
+            res.append(pt)
+            if verbose:
+                print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in pt.items()}),
+                      flush=True)
         del buf
         torch.cuda.empty_cache()
     return res
@@ -182,7 +203,7 @@ def run_study(name, quick, cal):
                 "high_lambda_rs": lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)}
     if name.startswith("gpt3_"):
         pat = name[len("gpt3_"):]
-        return {} if quick else {f"gpt3_4to1_{pat}": gpt3_study((pat,), True)}
+        return {} if quick else {f"gpt3_4to1_{pat}": gpt3_study((pat,), True, cal)}
     raise ValueError(name)
 
 

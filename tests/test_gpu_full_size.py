@@ -60,11 +60,14 @@ def rs_rows_reference(inp: dict, rows: np.ndarray) -> np.ndarray:
 
 
 def split_boundary_rows(inp: dict, frac_bwd: float) -> np.ndarray:
-    """The last backward-ring row and the first forward-ring row of every
-    chunk under a rate-proportional split (rounded to 8 rows)."""
+    """Rows on both sides of the candidate boundaries of a rate-proportional
+    split of every chunk (the exact share, and its roundings to 8 and to 128
+    rows)."""
     rows = inp["M"] // inp["n"]
-    h0 = int(round(rows * frac_bwd / 8.0)) * 8
-    return np.array([c * rows + h0 + o for c in range(inp["n"]) for o in (-1, 0)], dtype=np.int64)
+    x = rows * frac_bwd
+    cands = {int(x), int(round(x / 8.0)) * 8, int(x // 128) * 128, -(-int(x) // 128) * 128}
+    return np.array(sorted({c * rows + h + o for c in range(inp["n"]) for h in cands for o in (-1, 0)
+                            if 0 < h < rows}), dtype=np.int64)
 
 
 def check_ag(case: AGCase, inp: dict, parts: int, seed: int, extra_rows=None):
