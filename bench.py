@@ -296,11 +296,25 @@ def cpu_baseline(ag_in, rs_in) -> dict:
 
     import oracle as O
 
+    blas = "unknown"
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        if info:
+            blas = f"{info[0].get('internal_api', '?')} {info[0].get('version', '')}".strip()
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+        threadpool_limits = None
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
     n = ag_in["n"]
     rows = 256
     sh = [s[:rows] for s in ag_in["shards"]]
@@ -321,9 +335,22 @@ def cpu_baseline(ag_in, rs_in) -> dict:
         if time.perf_counter() - t_all > 10.0 or len(times) >= 50:
             break
     t = float(np.median(times))
+    # the same sample on one thread (a few runs)
+    t1 = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1, user_api="blas"):
+            one = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                O.ag_gemm([O.bf16_to_f64(s) for s in sh], O.bf16_to_f64(W1))
+                O.gemm_rs(O.bf16_to_f64(A2), O.bf16_to_f64(W2), [p.astype(np.float64) for p in P2], n)
+                one.append(time.perf_counter() - t0)
+            t1 = float(np.median(one))
     return {"value": round(flops / t / 1e12, 5), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{rows} rows of each of the {n} fc1 shards and fc2 chunks (1/{rows2 // rows} of a step), "
-                      f"fp64 numpy, median of {len(times)} runs"}
+                      f"fp64 numpy, median of {len(times)} runs",
+            "seconds": round(t, 4), "cpu_model": cpu_model, "blas": blas,
+            "value_1_thread": None if t1 is None else round(flops / t1 / 1e12, 5)}
 
 
 if __name__ == "__main__":
