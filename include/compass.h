@@ -72,6 +72,23 @@ extern "C" {
                                   InterDecom sub-operators split each piece
                                   the same way. Model: a step carries m/n over
                                   both rings at B_fwd + B_bwd. */
+#define COMPASS_RING_ALLTOALL 3  /* not a ring: the direct-push AlltoAll pattern the
+                                  paper compares its rings against (Section III-A),
+                                  AllGather only, n even, fused operator, transfer
+                                  and unfused baseline (InterDecom and the selector
+                                  return COMPASS_ERR_UNSUPPORTED). Ranks [0, n/2)
+                                  and [n/2, n) are two NUMA domains. Every peer of
+                                  this rank's domain pushes its chunk at the same
+                                  time over a link of its own at fwd_Bps; the n/2
+                                  peers of the other domain push at the same time
+                                  over the cross-domain link of bwd_Bps, which the
+                                  (n/2)^2 flows into this domain share equally, so
+                                  their chunks land together after
+                                  (n/2)^2 (m/n) / bwd_Bps (effective B/2 at n = 8,
+                                  against the single ring's 8/7 B over the same
+                                  link). Order: own chunk, the own domain's peers
+                                  in rank order from r + 1, then the other domain's
+                                  in rank order. */
 
 #define COMPASS_INTRA_FUSION 0  /* TA-IntraFusion  (Algorithm 1) */
 #define COMPASS_INTER_DECOM  1  /* ODP-InterDecom  (Algorithm 1) */
@@ -108,12 +125,24 @@ int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int c
  *
  * slice_bytes: largest single copy (0: library default, 2 MiB; else
  * >= 4 KiB). engines_per_ring: SDMA engines per ring direction (0: library
- * default, all usable engines split over the active directions). */
+ * default, all usable engines split over the active directions).
+ *
+ * hop_Bps (single ring only; NULL: every hop at fwd_Bps): n rates, hop q
+ * carrying rank q -> q+1 mod n, each >= 1e8 (paced), for a ring whose hops
+ * differ, as on the cross-NUMA ring of Section III-A. The ring then has no
+ * step barrier: item s reaches this rank at the time
+ * compass_ring_arrival_times gives (store and forward, one item per hop at
+ * a time, the emulated ranks forwarding as soon as they hold an item). The
+ * incoming items take the rate of the hop into this rank, the ReduceScatter
+ * sums sent onward that of the hop out of it. The caller owns the array; it
+ * is read during the call only. Another ring with hop_Bps set returns
+ * COMPASS_ERR_UNSUPPORTED. */
 typedef struct compass_links {
     double fwd_Bps;
     double bwd_Bps;
     size_t slice_bytes;
     int    engines_per_ring;
+    const double *hop_Bps;
 } compass_links;
 
 /* ---- one operator instance ----------------------------------------------
@@ -278,7 +307,7 @@ typedef struct compass_workload {   /* W of Eq. 1 / Eq. 6 */
 } compass_workload;
 
 typedef struct compass_topology {   /* T of Eq. 1 / Eq. 6 */
-    int    ring;                    /* COMPASS_RING_SINGLE / _DOUBLE          */
+    int    ring;                    /* COMPASS_RING_*                         */
     double fwd_Bps, bwd_Bps;        /* per-direction link rates, bytes/s      */
     double step_latency_s;          /* fixed cost of one ring step            */
 } compass_topology;
@@ -313,6 +342,28 @@ typedef struct compass_choice {     /* (S*, T*) of Algorithm 1, with details  */
  * ring: every half-chunk) evenly. Host only, O(1); needs no GPU. */
 int compass_pick_strategy(const compass_workload *w, const compass_topology *t,
                           const compass_calib *cal, compass_choice *out);
+
+/* T_comm of the whole collective under topology t, in seconds (host only):
+ * single / double ring as compass_pick_strategy computes it (n - 1 steps);
+ * COMPASS_RING_DOUBLE_SPLIT: n - 1 steps of the whole chunk at
+ * fwd_Bps + bwd_Bps; COMPASS_RING_ALLTOALL (AllGather, even n): one round,
+ * max((m/n) / fwd_Bps, (n/2)^2 (m/n) / bwd_Bps) + step_latency_s (the first
+ * term only for n > 2).
+ * Returns a negative value for a NULL argument, an unknown ring, n < 1 or a
+ * rate the ring needs that is not positive. */
+double compass_model_t_comm(const compass_workload *w, const compass_topology *t);
+
+/* Arrival times at `rank` of a single ring with per-hop rates (seconds
+ * from the start; the emulator's due times under compass_links.hop_Bps):
+ * hop q carries rank q -> q+1 mod n at hop_Bps[q]; every hop carries one
+ * piece of piece_bytes at a time; a rank forwards a piece once it holds it.
+ * d >= 1 sub-collectives (InterDecom) run one after another on the same
+ * hops. out[j*(n-1) + s-1] = arrival of step s (1..n-1) of sub-collective j.
+ * Returns d*(n-1), or a negative status (NULL pointers, n outside
+ * [1, 32], rank outside [0, n), d < 1, cap too small, a rate that is not
+ * positive and finite, piece_bytes < 0). Host only (Section III-A). */
+int compass_ring_arrival_times(int n, int rank, double piece_bytes, const double *hop_Bps, int d,
+                               double *out, int cap);
 
 /* Eq. 2 and Eq. 7-8 evaluated directly (host only). */
 double compass_model_t_decomp(double t_comp, double t_comm, int d, double alpha, double beta);

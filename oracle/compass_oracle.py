@@ -31,7 +31,9 @@ Contents
 Where the paper leaves a point open, the function states the reading it
 takes. ``DOUBLE_SPLIT`` (a double ring whose chunk rows are split between
 the directions in proportion to their rates) is not the paper's design,
-which splits every chunk in halves; it is an extension of it.
+which splits every chunk in halves; it is an extension of it. ``ALLTOALL``
+is the comparison pattern of Section III-A (every rank pushes its chunk to
+every other at once, two NUMA domains of n/2 ranks), AllGather only.
 
 Parity status
   * GEMM parts, schedules, ring bandwidths, Eq. 2-8 identities: pinned by
@@ -53,6 +55,7 @@ RS = "rs"
 SINGLE = "single"
 DOUBLE = "double"
 DOUBLE_SPLIT = "double_split"   # double ring, chunk rows split in proportion to the two rates
+ALLTOALL = "alltoall"           # direct pushes, two NUMA domains (AllGather only)
 
 # --------------------------------------------------------------------------
 # bf16 <-> fp64
@@ -212,6 +215,18 @@ def schedule(pattern: str, ring: str, n: int, r: int) -> list:
         for s in range(1, n):
             out.append(2 * ((r - s) % n) + 1)   # odd, forward ring, from r-1
             out.append(2 * ((r + s) % n))       # even, backward ring, from r+1
+    elif pattern == AG and ring == ALLTOALL:
+        # Reading: the paper fixes no arrival order for the AlltoAll pattern.
+        # The chunks of the own domain (direct fast links) come first, from
+        # r+1 onward within the domain, then the other domain's in rank order
+        # (they share the cross-domain link and land together).
+        if n % 2:
+            raise ValueError("AlltoAll needs an even n")
+        h = n // 2
+        d0 = (r // h) * h
+        out.append(r)
+        out += [d0 + (r - d0 + i) % h for i in range(1, h)]
+        out += [(d0 + h) % n + i for i in range(h)]
     elif pattern == RS and ring == SINGLE:
         for s in range(n):
             out.append((r - 1 - s) % n)         # local chunk r comes last
@@ -266,6 +281,77 @@ def simulate_ring_allgather(n: int, ring: str) -> list:
                 held[q].append(inbox_b[q])
                 last_bwd[q] = inbox_b[q]
     return held
+
+
+def ring_arrival_times(n: int, r: int, piece_bytes: float, hop_Bps: Sequence[float], d: int = 1) -> list:
+    """Arrival times at rank r of a single-ring collective whose hops run at
+    different rates (Section III-A: the cross-NUMA ring, where only some hops
+    cross the slow link). Hop q carries rank q -> q+1 at hop_Bps[q].
+
+    Reading: the ring has no global step barrier. Every hop carries one
+    piece at a time, and a rank forwards a piece once it holds all of it
+    (store and forward). So the piece rank q receives at step s is in
+    flight once the sender q-1 holds it (its own piece at s = 1, else its
+    arrival at step s-1) and the hop q-1 -> q has delivered the previous
+    piece, and it lands piece_bytes / hop_Bps[q-1] later. With d
+    sub-collectives (InterDecom), sub-collective j runs its n-1 steps after
+    j-1's on the same hops. The same times hold for the incoming running
+    sums of a ring ReduceScatter whose emulated ranks add instantly.
+
+    Returns d*(n-1) times, sub-collective-major, step s = 1..n-1 within."""
+    T = [piece_bytes / hop_Bps[q] for q in range(n)]
+    link_free = [0.0] * n          # the hop into rank q delivered its last piece
+    out = []
+    for _j in range(d):
+        held = [0.0] * n           # rank q holds the piece it forwards next
+        for _s in range(1, n):
+            now = [max(held[(q - 1) % n], link_free[q]) + T[(q - 1) % n] for q in range(n)]
+            link_free = now
+            held = now
+            out.append(now[r])
+    return out
+
+
+def simulate_timed_ring_allgather(n: int, chunk_bytes: float, hop_Bps: Sequence[float]) -> list:
+    """Event-driven simulation of a single-ring AllGather with per-hop
+    rates: every rank queues its own chunk on its outgoing hop; a hop sends
+    the pieces queued on it one at a time, first in first out; a rank that
+    receives a chunk records it and queues it onward unless the next rank is
+    the chunk's owner. Returns, per rank, the (time, chunk) arrivals in the
+    order they happen."""
+    import heapq
+    queue = [[(0.0, q)] if n > 1 else [] for q in range(n)]   # (ready time, chunk) waiting on hop q
+    busy_until = [0.0] * n
+    arrivals = [[] for _ in range(n)]
+    events = []                                # (time, seq, hop, chunk): hop delivers chunk
+    seq = 0
+
+    def start(q):
+        nonlocal seq
+        if not queue[q]:
+            return
+        ready, c = queue[q].pop(0)
+        t = max(ready, busy_until[q]) + chunk_bytes / hop_Bps[q]
+        busy_until[q] = t
+        heapq.heappush(events, (t, seq, q, c))
+        seq += 1
+
+    sending = [False] * n                      # a delivery of hop q is pending
+    for q in range(n):
+        start(q)
+        sending[q] = True
+    while events:
+        t, _, q, c = heapq.heappop(events)
+        sending[q] = False
+        dst = (q + 1) % n
+        arrivals[dst].append((t, c))
+        if (dst + 1) % n != c:
+            queue[dst].append((t, c))
+        for h in (q, dst):
+            if not sending[h] and queue[h]:
+                start(h)
+                sending[h] = True
+    return arrivals
 
 
 def simulate_ring_reduce_scatter(partials: Sequence[np.ndarray], ring: str):
@@ -358,6 +444,14 @@ def t_comm(pattern: str, ring: str, M: int, N: int, K: int, n: int,
     slowest active ring sets the pace (Section III-A). A per-step latency tau
     is added. Under ReduceScatter, the incoming and outgoing halves of a step
     use the two directions of the link and overlap."""
+    if ring == ALLTOALL:
+        # one round in which every flow runs at once (Section III-A)
+        if pattern != AG or n % 2:
+            raise ValueError("AlltoAll: AllGather over an even n only")
+        c_in, _ = comm_bytes_per_step(pattern, SINGLE, M, N, K, n, a_bytes, p_bytes, o_bytes)
+        h = n // 2
+        intra = c_in / fwd_Bps if h > 1 else 0.0     # n = 2: no peer inside a domain
+        return max(intra, h * h * c_in / bwd_Bps) + tau
     if ring == DOUBLE_SPLIT:
         # each step's chunk (m/n) is split between the rings in proportion to
         # their rates, so both rings finish the step together
@@ -369,6 +463,28 @@ def t_comm(pattern: str, ring: str, M: int, N: int, K: int, n: int,
     rates = [fwd_Bps] if ring == SINGLE else [fwd_Bps, bwd_Bps]
     step = max(max(b_in / r, b_out / r) for r in rates)
     return (n - 1) * (step + tau)
+
+
+def alltoall_link_time(n: int, chunk_bytes: float, intra_Bps: float, cross_Bps: float) -> float:
+    """Brute-force time of an AlltoAll AllGather on two NUMA domains of n/2
+    ranks (Section III-A): every rank sends its chunk to every other rank at
+    once. A pair inside one domain has a link of its own at ``intra_Bps``;
+    every flow from one domain to the other crosses that direction of the
+    single cross-domain link (``cross_Bps``). Flows on one link share it
+    equally, so the collective ends when the most loaded link has drained:
+    max over links of bytes / rate."""
+    h = n // 2
+    load = {}
+    for src in range(n):
+        for dst in range(n):
+            if src == dst:
+                continue
+            if src // h == dst // h:
+                link = ("intra", src, dst)
+            else:
+                link = ("cross", src // h, dst // h)
+            load[link] = load.get(link, 0.0) + chunk_bytes
+    return max(b / (intra_Bps if k[0] == "intra" else cross_Bps) for k, b in load.items())
 
 
 def effective_bandwidth(ring: str, n: int, B: float) -> float:

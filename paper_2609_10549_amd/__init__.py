@@ -16,6 +16,8 @@ from .compass import (  # noqa: F401
     compass_tile_trace,
     compass_probe_mfma,
     compass_last_error,
+    compass_model_t_comm,
+    compass_ring_arrival_times,
     compass_model_t_decomp,
     compass_model_t_fusion,
     compass_pick_strategy,

@@ -39,7 +39,9 @@ OPT_SCHED = 9
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RING_DOUBLE_SPLIT = 2
-RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE, "double_split": RING_DOUBLE_SPLIT}
+RING_ALLTOALL = 3
+RINGS = {"single": RING_SINGLE, "double": RING_DOUBLE, "double_split": RING_DOUBLE_SPLIT,
+         "alltoall": RING_ALLTOALL}
 
 
 class CompassError(RuntimeError):
@@ -50,7 +52,8 @@ class CompassError(RuntimeError):
 
 class compass_links(ctypes.Structure):
     _fields_ = [("fwd_Bps", ctypes.c_double), ("bwd_Bps", ctypes.c_double),
-                ("slice_bytes", ctypes.c_size_t), ("engines_per_ring", ctypes.c_int)]
+                ("slice_bytes", ctypes.c_size_t), ("engines_per_ring", ctypes.c_int),
+                ("hop_Bps", ctypes.POINTER(ctypes.c_double))]
 
 
 class compass_problem(ctypes.Structure):
@@ -113,6 +116,10 @@ _SIGS = {
     "compass_set_option": (ctypes.c_int, [ctypes.c_int, ctypes.c_longlong]),
     "compass_pick_strategy": (ctypes.c_int, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology),
                                              ctypes.POINTER(compass_calib), ctypes.POINTER(compass_choice)]),
+    "compass_ring_arrival_times": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                                  ctypes.POINTER(ctypes.c_double), ctypes.c_int,
+                                                  ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
+    "compass_model_t_comm": (ctypes.c_double, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology)]),
     "compass_model_t_decomp": (ctypes.c_double, [ctypes.c_double, ctypes.c_double, ctypes.c_int,
                                                  ctypes.c_double, ctypes.c_double]),
     "compass_model_t_fusion": (ctypes.c_double, [ctypes.POINTER(compass_workload), ctypes.c_double, ctypes.c_double,
@@ -210,9 +217,14 @@ def rs_problem(A, W, partial_src: Sequence, partial_stage, C, send_dst: Sequence
 
 
 def links(fwd_Bps: float = 0.0, bwd_Bps: float | None = None, slice_bytes: int = 0,
-          engines_per_ring: int = 0) -> compass_links:
-    return compass_links(fwd_Bps=fwd_Bps, bwd_Bps=fwd_Bps if bwd_Bps is None else bwd_Bps,
-                         slice_bytes=slice_bytes, engines_per_ring=engines_per_ring)
+          engines_per_ring: int = 0, hop_Bps: Sequence[float] | None = None) -> compass_links:
+    lk = compass_links(fwd_Bps=fwd_Bps, bwd_Bps=fwd_Bps if bwd_Bps is None else bwd_Bps,
+                       slice_bytes=slice_bytes, engines_per_ring=engines_per_ring)
+    if hop_Bps is not None:
+        arr = (ctypes.c_double * len(hop_Bps))(*hop_Bps)
+        lk.hop_Bps = arr
+        lk._hops = arr   # kept alive with the struct
+    return lk
 
 
 def _lk(lk) -> compass_links:
@@ -293,6 +305,20 @@ def compass_pick_strategy(workload: compass_workload, topology: compass_topology
     _check(lib().compass_pick_strategy(ctypes.byref(workload), ctypes.byref(topology), ctypes.byref(calib),
                                        ctypes.byref(out)), "compass_pick_strategy")
     return out
+
+
+def compass_ring_arrival_times(n: int, rank: int, piece_bytes: float, hop_Bps: Sequence[float],
+                               d: int = 1) -> list:
+    hops = (ctypes.c_double * max(n, 1))(*list(hop_Bps)[:max(n, 1)])
+    cap = max(1, d * max(n - 1, 0))
+    out = (ctypes.c_double * cap)()
+    k = _check(lib().compass_ring_arrival_times(n, rank, piece_bytes, hops, d, out, cap),
+               "compass_ring_arrival_times")
+    return list(out[:k])
+
+
+def compass_model_t_comm(workload: compass_workload, topology: compass_topology) -> float:
+    return lib().compass_model_t_comm(ctypes.byref(workload), ctypes.byref(topology))
 
 
 def compass_model_t_decomp(t_comp: float, t_comm: float, d: int, alpha: float, beta: float) -> float:

@@ -51,6 +51,22 @@ int compass_pick_strategy(const compass_workload *w, const compass_topology *t, 
     return pick(w, t, cal, out);
 }
 
+int compass_ring_arrival_times(int n, int rank, double piece_bytes, const double *hop_Bps, int d, double *out,
+                               int cap) {
+    return ring_arrivals(n, rank, piece_bytes, hop_Bps, d, out, cap);
+}
+
+double compass_model_t_comm(const compass_workload *w, const compass_topology *t) {
+    if (!w || !t || w->n < 1) return -1.0;
+    const int r = t->ring;
+    if (r != COMPASS_RING_SINGLE && r != COMPASS_RING_DOUBLE && r != COMPASS_RING_DOUBLE_SPLIT &&
+        r != COMPASS_RING_ALLTOALL)
+        return -1.0;
+    if (r == COMPASS_RING_ALLTOALL && (w->pattern != COMPASS_AG_GEMM || w->n % 2)) return -1.0;
+    if (!(t->fwd_Bps > 0) || (r != COMPASS_RING_SINGLE && !(t->bwd_Bps > 0))) return -1.0;
+    return model_t_comm(*w, *t);
+}
+
 double compass_model_t_decomp(double t_comp, double t_comm, int d, double alpha, double beta) {
     return model_t_decomp(t_comp, t_comm, d, alpha, beta);
 }

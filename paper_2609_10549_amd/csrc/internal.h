@@ -14,6 +14,8 @@ const char *last_error();
 int schedule_fill(int pattern, int ring, int n, int rank, int32_t *out, int cap);
 int pick(const compass_workload *w, const compass_topology *t, const compass_calib *cal, compass_choice *out);
 int calibrate(const compass_sample *s, int count, compass_calib *inout);
+double model_t_comm(const compass_workload &w, const compass_topology &t);
+int ring_arrivals(int n, int rank, double piece_bytes, const double *hop_Bps, int d, double *out, int cap);
 double model_t_decomp(double tc, double tm, int d, double alpha, double beta);
 double model_t_fusion(const compass_workload &w, double tc, double tm_step, double af, double bf);
 

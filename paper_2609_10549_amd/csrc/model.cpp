@@ -16,12 +16,24 @@ int schedule_fill(int pattern, int ring, int n, int rank, int32_t *out, int cap)
         return set_error(COMPASS_ERR_INVALID, "schedule: need 1 <= n <= 32 and 0 <= rank < n");
     if (pattern != COMPASS_AG_GEMM && pattern != COMPASS_GEMM_RS)
         return set_error(COMPASS_ERR_INVALID, "schedule: unknown pattern");
-    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE && ring != COMPASS_RING_DOUBLE_SPLIT)
+    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE && ring != COMPASS_RING_DOUBLE_SPLIT &&
+        ring != COMPASS_RING_ALLTOALL)
         return set_error(COMPASS_ERR_INVALID, "schedule: unknown ring");
-    const int len = ring == COMPASS_RING_SINGLE ? n : 2 * n;
+    const bool one = ring == COMPASS_RING_SINGLE || ring == COMPASS_RING_ALLTOALL;
+    const int len = one ? n : 2 * n;
     if (!out || cap < len) return set_error(COMPASS_ERR_INVALID, "schedule: output too small");
     auto md = [n](int x) { return ((x % n) + n) % n; };
     int k = 0;
+    if (ring == COMPASS_RING_ALLTOALL) {
+        if (pattern != COMPASS_AG_GEMM) return set_error(COMPASS_ERR_UNSUPPORTED, "schedule: AlltoAll is AllGather only");
+        if (n % 2) return set_error(COMPASS_ERR_INVALID, "schedule: AlltoAll needs an even n");
+        // own chunk, the own domain's peers from r + 1, then the other domain's
+        const int h = n / 2, d0 = rank / h * h;
+        out[k++] = rank;
+        for (int i = 1; i < h; ++i) out[k++] = d0 + (rank - d0 + i) % h;
+        for (int i = 0; i < h; ++i) out[k++] = (d0 + h) % n + i;
+        return k;
+    }
     if (pattern == COMPASS_AG_GEMM) {
         if (ring == COMPASS_RING_SINGLE) {
             // step s holds the chunk that travelled s hops on the forward ring
@@ -64,6 +76,14 @@ static void step_bytes(const compass_workload &w, int ring, double *in, double *
 
 double model_t_comm(const compass_workload &w, const compass_topology &t) {
     double in, out;
+    if (t.ring == COMPASS_RING_ALLTOALL) {
+        // every chunk at once: the own domain's over their own links, the other
+        // domain's (n/2)^2 flows sharing the cross-domain link
+        step_bytes(w, COMPASS_RING_SINGLE, &in, &out);
+        const double h = w.n / 2.0;
+        const double intra = w.n > 2 ? in / t.fwd_Bps : 0.0;   // n = 2: no peer inside a domain
+        return std::fmax(intra, h * h * in / t.bwd_Bps) + t.step_latency_s;
+    }
     if (t.ring == COMPASS_RING_DOUBLE_SPLIT) {
         // the step's whole chunk over both rings, each carrying its rate's share
         step_bytes(w, COMPASS_RING_SINGLE, &in, &out);
@@ -78,6 +98,35 @@ double model_t_comm(const compass_workload &w, const compass_topology &t) {
         step = std::fmax(step, std::fmax(in / r, out / r));
     }
     return (w.n - 1) * (step + t.step_latency_s);
+}
+
+int ring_arrivals(int n, int rank, double piece_bytes, const double *hop_Bps, int d, double *out, int cap) {
+    if (!hop_Bps || !out) return set_error(COMPASS_ERR_INVALID, "ring_arrival_times: NULL argument");
+    if (n < 1 || n > kMaxRanks || rank < 0 || rank >= n || d < 1)
+        return set_error(COMPASS_ERR_INVALID, "ring_arrival_times: need 1 <= n <= %d, 0 <= rank < n, d >= 1", kMaxRanks);
+    if (!(piece_bytes >= 0) || !std::isfinite(piece_bytes))
+        return set_error(COMPASS_ERR_INVALID, "ring_arrival_times: bad piece size");
+    for (int q = 0; q < n; ++q)
+        if (!(hop_Bps[q] > 0) || !std::isfinite(hop_Bps[q]))
+            return set_error(COMPASS_ERR_INVALID, "ring_arrival_times: hop %d rate must be positive", q);
+    const long total = (long)d * (n - 1);
+    if (cap < total) return set_error(COMPASS_ERR_INVALID, "ring_arrival_times: output too small");
+    // into[q]: when the hop into rank q delivered its last piece;
+    // has[q]: when rank q holds the piece it forwards at the next step
+    double into[kMaxRanks] = {}, has[kMaxRanks], nxt[kMaxRanks];
+    int k = 0;
+    for (int j = 0; j < d; ++j) {
+        for (int q = 0; q < n; ++q) has[q] = 0.0;   // every rank's own piece of sub-collective j
+        for (int st = 1; st < n; ++st) {
+            for (int q = 0; q < n; ++q) {
+                const int from = (q + n - 1) % n;
+                nxt[q] = std::fmax(has[from], into[q]) + piece_bytes / hop_Bps[from];
+            }
+            for (int q = 0; q < n; ++q) into[q] = has[q] = nxt[q];
+            out[k++] = nxt[rank];
+        }
+    }
+    return k;
 }
 
 double model_t_comp(const compass_workload &w, const compass_calib &c) {
@@ -129,6 +178,8 @@ int pick(const compass_workload *w, const compass_topology *t, const compass_cal
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: bad workload");
     if (w->pattern != COMPASS_AG_GEMM && w->pattern != COMPASS_GEMM_RS)
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown pattern");
+    if (t->ring == COMPASS_RING_ALLTOALL)
+        return set_error(COMPASS_ERR_UNSUPPORTED, "pick_strategy: the models are for rings");
     if (t->ring != COMPASS_RING_SINGLE && t->ring != COMPASS_RING_DOUBLE && t->ring != COMPASS_RING_DOUBLE_SPLIT)
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: unknown ring");
     if (!(t->fwd_Bps > 0) || (t->ring != COMPASS_RING_SINGLE && !(t->bwd_Bps > 0)))

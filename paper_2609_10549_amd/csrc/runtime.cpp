@@ -98,6 +98,7 @@ struct Item {
     hsa_agent_t dst_agent, src_agent;
     int flag;   // arrival flag to publish after the item, -1: none
     int gate;   // host done flag to wait for before the item, -1: none
+    double due_at = -1.0;   // paced, >= 0: due this long after the job started
 };
 
 struct Job {
@@ -107,6 +108,7 @@ struct Job {
     size_t slice = kDefaultSlice;
     uint32_t epoch = 0;
     bool wait_start = true;
+    bool concurrent = false;         // paced: every item on a link of its own
     int final_flag = -1;             // flag published after every item landed
 };
 
@@ -436,6 +438,13 @@ static size_t group_width(double rate, size_t E, size_t item_bytes) {
 // whichever is later. The kernel therefore never sees data before the link
 // would have delivered it.
 //
+// Concurrent (paced): every item has a link of its own at `rate`, all of them
+// starting with the job (or at the item's gate), so item i is due at
+// start + bytes / rate and the link_free chain is not advanced.
+//
+// An item with a due time of its own (due_at >= 0, paced) is due that long
+// after the job started, whatever the chain says (a ring whose hops differ).
+//
 // Unpaced (rate <= 0): slices go out round-robin over the engines as fast as
 // they are taken; an item's flag is published when its slices have landed.
 //
@@ -461,11 +470,15 @@ void Pacer::execute(Job &job) {
     const bool paced = job.rate > 0;
     size_t max_item = 0;
     for (auto &it : job.items) max_item = std::max(max_item, it.bytes);
-    const size_t k = paced ? group_width(job.rate, E, max_item) : E;
+    // concurrent items each take a group of their own where the engines allow
+    const size_t k = !paced ? E
+                     : job.concurrent ? std::max<size_t>(1, E / std::max<size_t>(1, job.items.size()))
+                                      : group_width(job.rate, E, max_item);
     const size_t groups = E / k;
     std::vector<hsa_signal_t> issued;
     std::vector<Pend> pend;
     double link_free = now_s();
+    const double job_start = link_free;
     double last_progress = link_free;
     size_t rr = 0, idx = 0, off = 0, item_first = 0;
     bool gate_ok = false;
@@ -493,8 +506,8 @@ void Pacer::execute(Job &job) {
             Pend &pd = pend[i];
             if (!pd.landed) {
                 bool landed = true;
-                for (size_t q = pd.first; q < pd.first + pd.count && landed; ++q)
-                    landed = hsa_signal_load_scacquire(issued[q]) <= 0;
+                for (size_t si = pd.first; si < pd.first + pd.count && landed; ++si)
+                    landed = hsa_signal_load_scacquire(issued[si]) <= 0;
                 if (landed) {
                     pd.landed = true;
                     if (paced && pd.model > 0) {
@@ -524,7 +537,7 @@ void Pacer::execute(Job &job) {
             if (it.gate < 0 || gate_ok) {
                 if (paced) {
                     const double start = std::max(link_free, it.gate >= 0 ? gate_time : 0.0);
-                    const double due = start + (double)it.bytes / job.rate;
+                    const double due = it.due_at >= 0 ? job_start + it.due_at : start + (double)it.bytes / job.rate;
                     const double model = kCopyFixed + (double)it.bytes / ((double)k * kEngineBps);
                     if (now_s() >= due - model * lat_scale) {
                         const size_t first = issued.size();
@@ -538,7 +551,7 @@ void Pacer::execute(Job &job) {
                             o += len;
                         }
                         if (it.flag >= 0) pend.push_back({it.flag, first, issued.size() - first, due, now_s(), model, false});
-                        link_free = due;
+                        if (!job.concurrent) link_free = due;
                         ++idx;
                         gate_ok = false;
                         progress = true;
@@ -650,6 +663,11 @@ static std::vector<uint32_t> engines_for(int role, const std::vector<int> &activ
     return out;
 }
 
+// The paper's double ring in either split (two partitions per chunk).
+static inline bool two_rings(const compass_problem *p) {
+    return p->ring == COMPASS_RING_DOUBLE || p->ring == COMPASS_RING_DOUBLE_SPLIT;
+}
+
 struct Geometry {
     int P;           // partitions
     int rows;        // rows per chunk
@@ -697,12 +715,17 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     if (!l) return set_error(COMPASS_ERR_INVALID, "links is NULL");
     if (want_pattern >= 0 && p->pattern != want_pattern) return set_error(COMPASS_ERR_INVALID, "wrong pattern for this call");
     if (p->pattern != COMPASS_AG_GEMM && p->pattern != COMPASS_GEMM_RS) return set_error(COMPASS_ERR_INVALID, "unknown pattern");
-    if (p->ring != COMPASS_RING_SINGLE && p->ring != COMPASS_RING_DOUBLE && p->ring != COMPASS_RING_DOUBLE_SPLIT)
+    if (p->ring != COMPASS_RING_SINGLE && p->ring != COMPASS_RING_DOUBLE && p->ring != COMPASS_RING_DOUBLE_SPLIT &&
+        p->ring != COMPASS_RING_ALLTOALL)
         return set_error(COMPASS_ERR_INVALID, "unknown ring");
     if (p->n < 1 || p->n > kMaxRanks || p->rank < 0 || p->rank >= p->n)
         return set_error(COMPASS_ERR_INVALID, "need 1 <= n <= %d and 0 <= rank < n", kMaxRanks);
+    if (p->ring == COMPASS_RING_ALLTOALL) {
+        if (p->pattern != COMPASS_AG_GEMM) return set_error(COMPASS_ERR_UNSUPPORTED, "the AlltoAll pattern is AllGather only");
+        if (p->n % 2) return set_error(COMPASS_ERR_INVALID, "the AlltoAll pattern needs an even n");
+    }
     if (p->M < 1 || p->N < 1 || p->K < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
-    const int P = p->ring == COMPASS_RING_SINGLE ? p->n : 2 * p->n;
+    const int P = two_rings(p) ? 2 * p->n : p->n;
     if (p->M % P) return set_error(COMPASS_ERR_INVALID, "M must be divisible by %d", P);
     if (p->K % 8 || p->N % 8) return set_error(COMPASS_ERR_INVALID, "K and N must be multiples of 8");
     if ((p->M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
@@ -727,10 +750,16 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     for (double r : {l->fwd_Bps, l->bwd_Bps})
         if (!std::isfinite(r) || (r > 0 && r < 1e8))
             return set_error(COMPASS_ERR_INVALID, "link rates must be <= 0 (unpaced) or at least 1e8 bytes/s");
+    if (l->hop_Bps) {
+        if (p->ring != COMPASS_RING_SINGLE) return set_error(COMPASS_ERR_UNSUPPORTED, "per-hop rates need the single ring");
+        for (int q = 0; q < p->n; ++q)
+            if (!std::isfinite(l->hop_Bps[q]) || l->hop_Bps[q] < 1e8)
+                return set_error(COMPASS_ERR_INVALID, "hop %d: per-hop rates must be at least 1e8 bytes/s", q);
+    }
     g->P = P;
     g->rows = p->M / p->n;
     g->prow = p->M / P;
-    g->dbl = p->ring != COMPASS_RING_SINGLE;
+    g->dbl = two_rings(p);
     g->fb = 0.5;
     if (p->ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0)
         g->fb = l->bwd_Bps / (l->fwd_Bps + l->bwd_Bps);
@@ -788,8 +817,12 @@ static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.
 static double lambda_estimate(const compass_problem *p, const Geometry &geo, const compass_links *l) {
     const double flops = 2.0 * p->M * (double)p->N * p->K;
     double step = p->pattern == COMPASS_AG_GEMM ? (double)geo.prow * p->K * 2 : (double)geo.prow * p->N * 4;
-    const bool dbl = p->ring != COMPASS_RING_SINGLE;
+    const bool dbl = two_rings(p);
     double rate = dbl ? std::fmin(l->fwd_Bps, l->bwd_Bps) : l->fwd_Bps;
+    if (l->hop_Bps) {
+        rate = l->hop_Bps[0];
+        for (int q = 1; q < p->n; ++q) rate = std::fmin(rate, l->hop_Bps[q]);
+    }
     if (p->ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0) {
         step *= 2.0;                        // the whole chunk per step ...
         rate = l->fwd_Bps + l->bwd_Bps;     // ... over both rings at once
@@ -908,12 +941,12 @@ static hipError_t copy_if_needed(void *dst, const void *src, size_t bytes, hipSt
 }
 
 // Partition p's rows (identity map): chunk c = p (single) or p / 2 (double).
-static inline int part_chunk(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE ? q : q / 2; }
-static inline int part_half(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE ? 0 : q % 2; }
-static inline bool part_fwd(const compass_problem *p, int q) { return p->ring == COMPASS_RING_SINGLE || (q % 2) == 1; }
+static inline int part_chunk(const compass_problem *p, int q) { return two_rings(p) ? q / 2 : q; }
+static inline int part_half(const compass_problem *p, int q) { return two_rings(p) ? q % 2 : 0; }
+static inline bool part_fwd(const compass_problem *p, int q) { return !two_rings(p) || (q % 2) == 1; }
 // Rows [*off, *off + *cnt) of a block of r chunk rows that partition half h carries.
 static inline void part_rows(const compass_problem *p, const Geometry &g, int r, int h, int *off, int *cnt) {
-    if (p->ring == COMPASS_RING_SINGLE) { *off = 0; *cnt = r; return; }
+    if (!two_rings(p)) { *off = 0; *cnt = r; return; }
     const int h0 = half0(g, r);
     *off = h ? h0 : 0;
     *cnt = h ? r - h0 : h0;
@@ -939,6 +972,17 @@ static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, i
     j.engines = engines_for(role, active, weight, l->engines_per_ring);
 }
 
+// Per-hop rates: the due times of the d * (n - 1) items this rank receives
+// (sub-collective-major) for pieces of `piece_bytes`; empty without hop rates.
+static int hop_arrivals(const compass_problem *p, const compass_links *l, int d, double piece_bytes,
+                        std::vector<double> *out) {
+    out->clear();
+    if (!l->hop_Bps || p->n < 2) return COMPASS_OK;
+    out->resize((size_t)d * (p->n - 1));
+    const int k = ring_arrivals(p->n, p->rank, piece_bytes, l->hop_Bps, d, out->data(), (int)out->size());
+    return k < 0 ? k : COMPASS_OK;
+}
+
 // ---------------------------------------------------------------- AllGather jobs
 // Items: the remote partitions in schedule order (the local ones are already
 // in place); forward-ring partitions go to role 0, backward-ring to role 1.
@@ -946,13 +990,27 @@ static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, i
 // with flags j * P + partition.
 static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    bool wait_start, Job *fwd, Job *bwd) {
+    const bool a2a = p->ring == COMPASS_RING_ALLTOALL;
+    const int dom = std::max(1, p->n / 2);                          // AlltoAll: ranks per NUMA domain
     const std::vector<int> active = p->ring == COMPASS_RING_SINGLE ? std::vector<int>{0} : std::vector<int>{0, 1};
-    const std::vector<int> weight(active.size(), 1);
+    // AlltoAll: role 0 carries the dom - 1 chunks of this rank's domain, role 1
+    // the dom chunks of the other domain
+    const std::vector<int> weight = a2a ? std::vector<int>{std::max(1, dom - 1), dom} : std::vector<int>(active.size(), 1);
     fill_job(*fwd, l, true, epoch, 0, active, weight);
     fill_job(*bwd, l, false, epoch, 1, active, weight);
     fwd->wait_start = bwd->wait_start = wait_start;
+    if (a2a) {
+        // every flow at once; the dom * dom flows into this domain share the
+        // cross-domain link equally
+        fwd->concurrent = bwd->concurrent = true;
+        if (bwd->rate > 0) bwd->rate /= (double)dom * dom;
+    }
     const size_t K = (size_t)p->K;
     const int pc = geo.rows / d;                                     // chunk rows per sub-operator
+    std::vector<double> due;
+    int rc0 = hop_arrivals(p, l, d, (double)pc * K * 2, &due);
+    if (rc0 != COMPASS_OK) return rc0;
+    if (!due.empty()) fwd->rate = l->hop_Bps[(p->rank + p->n - 1) % p->n];   // the hop into this rank
     for (int j = 0; j < d; ++j) {
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
@@ -968,7 +1026,9 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      (const char *)p->shard_src[c] + row_in_chunk * K * 2, (size_t)piece * K * 2,
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
-            (part_fwd(p, q) ? fwd : bwd)->items.push_back(it);
+            if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s
+            const bool on_fwd = a2a ? (c / dom == p->rank / dom) : part_fwd(p, q);
+            (on_fwd ? fwd : bwd)->items.push_back(it);
         }
     }
     return COMPASS_OK;
@@ -982,7 +1042,7 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                    uint64_t resident, bool gate_out, bool wait_start, Job jobs[4]) {
     // incoming fp32 partials carry twice the bytes of the outgoing bf16 sums
     std::vector<int> active{0}, weight{2};
-    const bool dbl = p->ring != COMPASS_RING_SINGLE;
+    const bool dbl = two_rings(p);
     if (dbl) { active.push_back(1); weight.push_back(2); }
     if (p->send_dst) {
         active.push_back(2); weight.push_back(1);
@@ -994,6 +1054,13 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
     }
     const size_t N = (size_t)p->N;
     const int pc = geo.rows / d;
+    std::vector<double> due;
+    int rc0 = hop_arrivals(p, l, d, (double)pc * N * 4, &due);
+    if (rc0 != COMPASS_OK) return rc0;
+    if (!due.empty()) {
+        jobs[0].rate = l->hop_Bps[(p->rank + p->n - 1) % p->n];   // the hop into this rank ...
+        jobs[2].rate = l->hop_Bps[p->rank];                       // ... and out of it
+    }
     for (int j = 0; j < d; ++j) {
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
@@ -1008,6 +1075,7 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      (const char *)p->partial_src[c] + row_in_chunk * N * 4, (size_t)piece * N * 4,
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
+            if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s >= 1
             jobs[part_fwd(p, q) ? 0 : 1].items.push_back(it);
         }
         if (!p->send_dst) continue;
@@ -1034,10 +1102,10 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
 
 static uint64_t resident_mask(const compass_problem *p, const Geometry &geo) {
     if (p->pattern == COMPASS_AG_GEMM) {
-        if (p->ring == COMPASS_RING_SINGLE) return 1ull << p->rank;
+        if (!two_rings(p)) return 1ull << p->rank;
         return 3ull << (2 * p->rank);
     }
-    if (p->ring == COMPASS_RING_SINGLE) return 1ull << geo.sched[0];
+    if (!two_rings(p)) return 1ull << geo.sched[0];
     return (1ull << geo.sched[0]) | (1ull << geo.sched[1]);
 }
 
@@ -1090,10 +1158,10 @@ static int launch(const GemmParams &g0, int cfg, bool rs, hipStream_t s) {
                                           (uint64_t)c.trace_used + (uint64_t)g0.tiles_m * g0.tiles_n * g0.ksplit);
     }
     const bool timed = c.timing && c.timed_count < Ctx::kTimed;
-    if (timed) hipEventRecord(c.ev_begin[c.timed_count], s);
+    if (timed) (void)hipEventRecord(c.ev_begin[c.timed_count], s);
     const hipError_t e = launch_gemm(g, cfg, rs, s);
     if (e != hipSuccess) return hip_fail(e, "GEMM launch");
-    if (timed) hipEventRecord(c.ev_end[c.timed_count++], s);
+    if (timed) (void)hipEventRecord(c.ev_end[c.timed_count++], s);
     return COMPASS_OK;
 }
 
@@ -1259,6 +1327,8 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
     if (rc != COMPASS_OK) return rc;
     if (d < 1 || (d & (d - 1)) || geo.prow % d)
         return set_error(COMPASS_ERR_INVALID, "d must be a power of two dividing %d", geo.prow);
+    if (d > 1 && p->ring == COMPASS_RING_ALLTOALL)
+        return set_error(COMPASS_ERR_UNSUPPORTED, "InterDecom runs over the rings only");
     if (d * geo.P > kFinalFlag0) return set_error(COMPASS_ERR_UNSUPPORTED, "d * partitions exceeds the flag slots");
     if ((rc = begin()) != COMPASS_OK) return rc;
     hipStream_t s = (hipStream_t)stream;

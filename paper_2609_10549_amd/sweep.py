@@ -19,6 +19,12 @@
 * The GPT-3 175B shapes (8192 tokens, hidden 12288, TP = 8) over a double
   ring whose directions run at 4 : 1, with chunks split in halves and split
   in proportion to the rates (fused, unfused, InterDecom d = 2, 4, 8).
+* Cross-NUMA AllGather (Section III-A): the fc1 shape over two NUMA domains
+  of four ranks, the single ring (every step at the cross-domain rate B, and
+  with per-hop rates: two slow hops at B, the rest at 200 GB/s) against the
+  AlltoAll pattern (own-domain links at 200 GB/s, all cross-domain flows
+  sharing B): transfer alone, fused and unfused, their effective bandwidths
+  and the model's T_comm.
 * torch.matmul (hipBLASLt) on every GEMM shape, for context.
 
 Timing only: the inputs are seeded random bf16 on the GPU (parity is the
@@ -184,7 +190,57 @@ def gpt3_study(pats, verbose, cal=None):
     return res
 
 
-STUDIES = ("decomp", "mlp", "high", "gpt3_ag", "gpt3_rs")
+NUMA_INTRA_BPS = 200e9
+NUMA_CROSS_BPS = (50e9, 100e9)
+
+
+def numa_study(verbose):
+    """The single ring against the AlltoAll pattern on the cross-NUMA
+    topology of Section III-A (n = 8, two domains of four ranks), on the
+    fc1 AllGather shape. Single ring: every step at the cross-domain rate B
+    (its slowest hop; the paper's step model), and with per-hop rates (hops
+    3 -> 4 and 7 -> 0 at B, the rest at 200 GB/s) seen from rank 0, right
+    after a slow hop, and from rank 3, three fast hops downstream of one.
+    AlltoAll: own-domain chunks over direct links at 200 GB/s while the 16
+    flows into the domain share B."""
+    import types
+    pat, M, N, K, n = "ag", 8192, 2048, 4096, 8
+    S = M * K * 2.0
+    res = []
+    bufs = {r: CAL.Buffers(pat, M, N, K, n, "single", rank=r) for r in (0, 3)}
+    for cross in NUMA_CROSS_BPS:
+        hops = [cross if q in (3, 7) else NUMA_INTRA_BPS for q in range(n)]
+        cases = (("single", 0, "single", C.links(cross, cross)),
+                 ("single_hops", 0, "single", C.links(NUMA_INTRA_BPS, hop_Bps=hops)),
+                 ("single_hops", 3, "single", C.links(NUMA_INTRA_BPS, hop_Bps=hops)),
+                 ("alltoall", 0, "alltoall", C.links(NUMA_INTRA_BPS, cross)))
+        for name, rank, ring, lk in cases:
+            buf = bufs[rank]
+            prob = buf.problem if ring == "single" else \
+                C.ag_problem(buf.shards, buf.gathered, buf.W, buf.C, rank, ring)
+            view = types.SimpleNamespace(A=buf.A, W=buf.W, C=buf.C, P=buf.P, problem=prob)
+            pt = overlap_point(view, pat, lk, reps=5)
+            if name == "single_hops":
+                model = C.compass_ring_arrival_times(n, rank, S / n, hops)[-1]
+            else:
+                w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+                t = C.compass_topology(ring=C.RINGS[ring], fwd_Bps=lk.fwd_Bps, bwd_Bps=lk.bwd_Bps,
+                                       step_latency_s=0.0)
+                model = C.compass_model_t_comm(w, t)
+            pt.update(pattern=pat, ring=name, rank=rank, M=M, N=N, K=K, n=n, cross_Bps=cross,
+                      intra_Bps=cross if name == "single" else NUMA_INTRA_BPS,
+                      model_t_comm_us=model * 1e6, eff_bw_Bps=S / (pt["t_xfer_us"] * 1e-6),
+                      eff_bw_model_Bps=S / model)
+            res.append(pt)
+            if verbose:
+                print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in pt.items()}),
+                      flush=True)
+    del bufs
+    torch.cuda.empty_cache()
+    return res
+
+
+STUDIES = ("decomp", "mlp", "high", "gpt3_ag", "gpt3_rs", "numa")
 
 
 def run_study(name, quick, cal):
@@ -201,6 +257,8 @@ def run_study(name, quick, cal):
             return {}
         return {"high_lambda_ag": lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True),
                 "high_lambda_rs": lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)}
+    if name == "numa":
+        return {"numa_single_vs_alltoall": numa_study(True)}
     if name.startswith("gpt3_"):
         pat = name[len("gpt3_"):]
         return {} if quick else {f"gpt3_4to1_{pat}": gpt3_study((pat,), True, cal)}

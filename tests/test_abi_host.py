@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_sizes_match_c_layout():
-    assert ctypes.sizeof(C.compass_links) == 32
+    assert ctypes.sizeof(C.compass_links) == 40
     assert ctypes.sizeof(C.compass_problem) == 4 * 7 + 4 + 8 * 8
     assert ctypes.sizeof(C.compass_calib) == 6 * 8 + 8
     assert ctypes.sizeof(C.compass_choice) == 3 * 4 + 4 + 7 * 8
@@ -44,6 +44,78 @@ def test_schedule_bit_exact_vs_oracle(pattern, ring):
     for n in [1, 2, 3, 4, 5, 8, 16, 32]:
         for r in range(n):
             assert C.compass_schedule(pattern, ring, n, r) == O.schedule(pattern, ring, n, r)
+
+
+def test_alltoall_schedule_bit_exact_vs_oracle():
+    for n in [2, 4, 6, 8, 16, 32]:
+        for r in range(n):
+            assert C.compass_schedule("ag", "alltoall", n, r) == O.schedule("ag", "alltoall", n, r)
+    with pytest.raises(C.CompassError) as e:
+        C.compass_schedule("rs", "alltoall", 8, 0)
+    assert e.value.code == C.ERR_UNSUPPORTED
+    with pytest.raises(C.CompassError):
+        C.compass_schedule("ag", "alltoall", 5, 0)
+
+
+def test_model_t_comm_matches_oracle_for_every_ring():
+    rng = random.Random(7)
+    for _ in range(300):
+        ring = rng.choice(["single", "double", "double_split", "alltoall"])
+        pat = "ag" if ring == "alltoall" else rng.choice(["ag", "rs"])
+        n = rng.choice([2, 4, 8, 16])
+        M, N, K = 2 * n * rng.randint(1, 64) * 8, rng.randint(1, 64) * 64, rng.randint(1, 64) * 64
+        fwd, bwd, tau = rng.uniform(1e9, 500e9), rng.uniform(1e9, 500e9), rng.uniform(0, 2e-5)
+        w = C.compass_workload(pattern=C.PATTERNS[pat], M=M, N=N, K=K, n=n)
+        t = C.compass_topology(ring=C.RINGS[ring], fwd_Bps=fwd, bwd_Bps=bwd, step_latency_s=tau)
+        assert _rel(C.compass_model_t_comm(w, t), O.t_comm(pat, ring, M, N, K, n, fwd, bwd, tau)) < 1e-12
+    w = C.compass_workload(pattern=C.PATTERNS["rs"], M=64, N=64, K=64, n=8)
+    t = C.compass_topology(ring=C.RINGS["alltoall"], fwd_Bps=1e9, bwd_Bps=1e9, step_latency_s=0)
+    assert C.compass_model_t_comm(w, t) < 0                      # AllGather only
+    w.pattern, t.bwd_Bps = C.PATTERNS["ag"], 0.0
+    assert C.compass_model_t_comm(w, t) < 0                      # needs the cross-domain rate
+    t.ring = 9
+    assert C.compass_model_t_comm(w, t) < 0
+
+
+def test_ring_arrival_times_match_oracle():
+    rng = random.Random(29)
+    for _ in range(200):
+        n = rng.choice([1, 2, 3, 4, 8, 16, 32])
+        d = rng.choice([1, 2, 4, 16])
+        hops = [rng.uniform(1e8, 500e9) for _ in range(n)]
+        b = rng.uniform(0, 64e6)
+        for r in {0, n - 1, rng.randrange(n)}:
+            got = C.compass_ring_arrival_times(n, r, b, hops, d)
+            ref = O.ring_arrival_times(n, r, b, hops, d)
+            assert len(got) == len(ref) == d * (n - 1)
+            assert all(_rel(x, y) < 1e-13 or x == y for x, y in zip(got, ref))
+    for args in ((0, 0, 1.0, [1e9], 1), (4, 4, 1.0, [1e9] * 4, 1), (4, 0, 1.0, [1e9] * 4, 0),
+                 (4, 0, 1.0, [1e9, 0.0, 1e9, 1e9], 1), (4, 0, -1.0, [1e9] * 4, 1),
+                 (4, 0, 1.0, [1e9, float("nan"), 1e9, 1e9], 1)):
+        with pytest.raises(C.CompassError):
+            C.compass_ring_arrival_times(*args)
+
+
+def test_hop_rates_refused_off_the_single_ring_or_out_of_range():
+    lib = C.lib()
+    for ring in (C.RING_DOUBLE, C.RING_DOUBLE_SPLIT, C.RING_ALLTOALL):
+        st, keep = _fake_problem(C.AG_GEMM, 64, 64, 64, 2, ring=ring)
+        lk = C.links(1e9, 1e9, hop_Bps=[1e9, 1e9])
+        assert lib.compass_ag_gemm(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_UNSUPPORTED
+    for pattern, call in ((C.AG_GEMM, lib.compass_ag_gemm), (C.GEMM_RS, lib.compass_gemm_rs)):
+        st, keep = _fake_problem(pattern, 64, 64, 64, 2)
+        for hops in ([1e9, 5e7], [1e9, float("inf")], [0.0, 1e9]):
+            lk = C.links(1e9, hop_Bps=hops)
+            assert call(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+
+
+def test_pick_strategy_refuses_alltoall():
+    w = C.compass_workload(pattern=C.PATTERNS["ag"], M=1024, N=64, K=64, n=8)
+    t = C.compass_topology(ring=C.RINGS["alltoall"], fwd_Bps=1e9, bwd_Bps=1e9, step_latency_s=0)
+    c = C.compass_calib(comp_a=0, comp_b=1e-12, alpha_decomp=1, beta_decomp=0.1, d_max=16)
+    with pytest.raises(C.CompassError) as e:
+        C.compass_pick_strategy(w, t, c)
+    assert e.value.code == C.ERR_UNSUPPORTED
 
 
 def test_schedule_errors():
@@ -214,6 +286,17 @@ def test_degenerate_and_oversized_problems_are_refused_before_enqueue(pattern):
     other = lib.compass_gemm_rs if pattern == C.AG_GEMM else lib.compass_ag_gemm
     assert other(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
     assert "" != C.lib().compass_last_error().decode()
+
+
+def test_alltoall_pattern_refusals_before_enqueue():
+    lib = C.lib()
+    lk = C.links(0.0, 0.0)
+    st, keep = _fake_problem(C.GEMM_RS, 64, 64, 64, 2, ring=C.RING_ALLTOALL)
+    assert lib.compass_gemm_rs(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_UNSUPPORTED
+    st, keep = _fake_problem(C.AG_GEMM, 96, 64, 64, 3, ring=C.RING_ALLTOALL)    # odd n
+    assert lib.compass_ag_gemm(ctypes.byref(st), ctypes.byref(lk), None) == C.ERR_INVALID
+    st, keep = _fake_problem(C.AG_GEMM, 64, 64, 64, 2, ring=C.RING_ALLTOALL)
+    assert lib.compass_decomp_gemm(ctypes.byref(st), 2, ctypes.byref(lk), None) == C.ERR_UNSUPPORTED
 
 
 def test_plain_gemm_refuses_degenerate_shapes():

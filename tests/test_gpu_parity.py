@@ -540,3 +540,144 @@ def test_proportional_split_shortens_a_4_to_1_transfer():
         t[ring] = min(times)
     _say("transfer halves / split", t)
     assert t["double_split"] < 0.75 * t["double"]
+
+
+# ------------------------------------------------------------ AlltoAll pattern (Section III-A)
+NUMA = C.links(200e9, 40e9)    # own-domain links, shared cross-domain link
+
+
+@pytest.mark.parametrize("n", [2, 4, 8])
+@pytest.mark.parametrize("paced", [True, False])
+def test_ag_gemm_alltoall_integer_exact_all_ranks(n, paced):
+    M, N, K = 64 * n, 264, 200
+    inp = make_int_ag_inputs(M, N, K, n, seed=90 + n)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    for r in range(n):
+        _say("ag alltoall int", n, r, paced)
+        case = AGCase(inp, r, "alltoall")
+        C.compass_ag_gemm(case.problem, NUMA if paced else C.links(0.0, 0.0))
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+        assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_alltoall_sequential_and_transfer():
+    n = 8
+    inp = make_ag_inputs(1024, 520, 1032, n, seed=93)
+    case = AGCase(inp, 5, "alltoall")
+    _say("alltoall sequential")
+    C.compass_sequential(case.problem, NUMA)
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+    case = AGCase(inp, 3, "alltoall")
+    C.compass_transfer(case.problem, NUMA)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+def test_alltoall_transfer_is_about_half_the_single_ring_across_numa():
+    # n = 8, 4 MiB chunks, cross-domain rate B = 40 GB/s: the single ring
+    # takes 7 steps at B (~734 us); under AlltoAll the 16 flows into a
+    # domain share B and land after 16 x 4 MiB / B (~1678 us), and none
+    # earlier
+    n = 8
+    inp = make_ag_inputs(4096, 64, 4096, n, seed=94)
+    chunk = 4096 // n * 4096 * 2
+    B = 40e9
+    t = {}
+    for ring, lk in (("single", C.links(B, B)), ("alltoall", C.links(200e9, B))):
+        case = AGCase(inp, 0, ring)
+        C.compass_transfer(case.problem, lk)
+        C.compass_sync()
+        times = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            C.compass_transfer(case.problem, lk)
+            b.record()
+            b.synchronize()
+            C.compass_sync()
+            times.append(a.elapsed_time(b) * 1e-3)
+        t[ring] = min(times)
+        assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+    _say("single ring / alltoall", t)
+    assert t["alltoall"] >= 0.98 * 16 * chunk / B
+    assert t["single"] >= 0.98 * 7 * chunk / B
+    assert 0.3 < t["single"] / t["alltoall"] < 0.6     # model: (1/2) / (8/7) = 0.4375
+
+
+# ------------------------------------------------------------ single ring with per-hop rates (Section III-A)
+def _cross_numa_hops(n, slow, fast):
+    # hops n/2-1 -> n/2 and n-1 -> 0 cross the NUMA boundary
+    return [slow if q in (n // 2 - 1, n - 1) else fast for q in range(n)]
+
+
+@pytest.mark.parametrize("n", [2, 4, 8])
+def test_ag_gemm_hop_ring_integer_exact_all_ranks(n):
+    M, N, K = 64 * n, 264, 200
+    inp = make_int_ag_inputs(M, N, K, n, seed=110 + n)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    lk = C.links(100e9, hop_Bps=_cross_numa_hops(n, 10e9, 100e9))
+    for r in range(n):
+        _say("ag hop ring int", n, r)
+        case = AGCase(inp, r, "single")
+        C.compass_ag_gemm(case.problem, lk)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+        for d in (2, 4):
+            case.C.zero_()
+            C.compass_decomp_gemm(case.problem, d, lk)
+            C.compass_sync()
+            assert np.array_equal(host_bits(case.C), ref), f"rank {r} d {d}"
+
+
+@pytest.mark.parametrize("n", [4, 8])
+def test_gemm_rs_hop_ring_integer_exact_all_ranks(n):
+    M, N, K = 64 * n, 136, 128
+    inp = make_int_rs_inputs(M, N, K, n, seed=120 + n)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    lk = C.links(100e9, hop_Bps=_cross_numa_hops(n, 10e9, 100e9))
+    prow = M // n
+    for r in range(n):
+        _say("rs hop ring int", n, r)
+        case = RSCase(inp, r, "single")
+        C.compass_gemm_rs(case.problem, lk)
+        C.compass_sync()
+        got = host_bits(case.C)
+        assert np.array_equal(got, ref), f"rank {r}"
+        for q, snd in enumerate(case.send):
+            if snd is not None:
+                assert np.array_equal(host_bits(snd), ref[q * prow:(q + 1) * prow]), (r, q)
+
+
+def test_hop_ring_transfer_follows_the_per_rank_arrival_times():
+    # n = 8, 4 MiB chunks, hops 3->4 and 7->0 at 20 GB/s, the rest at 200 GB/s:
+    # rank 0 (after a slow hop) waits 7 x 4 MiB / 20 GB/s; rank 3, three fast
+    # hops downstream of one, finishes after 4 slow and 3 fast chunk times
+    n = 8
+    inp = make_ag_inputs(4096, 64, 4096, n, seed=125)
+    chunk = 4096 // n * 4096 * 2
+    hops = _cross_numa_hops(n, 20e9, 200e9)
+    lk = C.links(200e9, hop_Bps=hops)
+    t = {}
+    for r in (0, 3):
+        case = AGCase(inp, r, "single")
+        C.compass_transfer(case.problem, lk)
+        C.compass_sync()
+        times = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            C.compass_transfer(case.problem, lk)
+            b.record()
+            b.synchronize()
+            C.compass_sync()
+            times.append(a.elapsed_time(b) * 1e-3)
+        t[r] = min(times)
+        want = O.ring_arrival_times(n, r, chunk, hops)[-1]
+        _say("hop ring rank", r, "transfer", t[r], "due", want)
+        assert t[r] >= 0.98 * want
+        assert t[r] < 1.25 * want + 1e-3
+        assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+    assert t[3] < 0.8 * t[0]

@@ -249,3 +249,104 @@ def test_proportional_double_ring_reduces_to_halves_at_equal_rates():
         f = rng.uniform(0.05, 1.0)
         assert O.t_comm(pat, O.DOUBLE_SPLIT, M, N, K, n, B, B * f) <= \
             O.t_comm(pat, O.DOUBLE, M, N, K, n, B, B * f) * (1 + 1e-12)
+
+
+def test_alltoall_closed_form_matches_brute_force_link_loads():
+    # the one-round closed form against the per-link loads of every flow
+    rng = random.Random(13)
+    for _ in range(60):
+        n = rng.choice([2, 4, 6, 8, 12, 16])
+        M, K = n * rng.randint(1, 64) * 8, rng.randint(1, 64) * 64
+        fwd, bwd = rng.uniform(1e9, 500e9), rng.uniform(1e9, 500e9)
+        chunk = M * K * 2 / n
+        want = O.alltoall_link_time(n, chunk, fwd, bwd)
+        assert O.t_comm(O.AG, O.ALLTOALL, M, 1, K, n, fwd, bwd) == pytest.approx(want, rel=1e-13)
+        assert O.t_comm(O.AG, O.ALLTOALL, M, 1, K, n, fwd, bwd, tau=2e-6) == pytest.approx(want + 2e-6, rel=1e-13)
+
+
+def test_alltoall_is_about_half_the_single_ring_across_numa():
+    # Section III-A: on the 8-GPU cross-NUMA topology the single ring reaches
+    # (8/7) B_QPI and the AlltoAll pattern B_QPI / 2, whatever the (faster)
+    # links inside a domain carry
+    B = 40e9
+    S = 8 * 8 * 1024 * 1024 * 2.0
+    for intra in (B, 200e9, 1e12):
+        t = O.t_comm(O.AG, O.ALLTOALL, 8 * 1024, 1, 8 * 1024, 8, intra, B)
+        assert S / t == pytest.approx(B / 2, rel=1e-12)
+    ring = O.t_comm(O.AG, O.SINGLE, 8 * 1024, 1, 8 * 1024, 8, B, B)
+    assert ring / t == pytest.approx((1 / 2) / (8 / 7), rel=1e-12)
+
+
+def test_alltoall_refuses_reducescatter_and_odd_n():
+    with pytest.raises(ValueError):
+        O.t_comm(O.RS, O.ALLTOALL, 64, 64, 64, 8, 1e9, 1e9)
+    with pytest.raises(ValueError):
+        O.t_comm(O.AG, O.ALLTOALL, 60, 64, 64, 3, 1e9, 1e9)
+    with pytest.raises(ValueError):
+        O.schedule(O.AG, O.ALLTOALL, 5, 0)
+
+
+# ---- single ring with per-hop rates (Section III-A, cross-NUMA ring)
+def test_hop_ring_uniform_rates_are_serialized_steps():
+    for n in (2, 3, 8, 16):
+        for r in range(n):
+            got = O.ring_arrival_times(n, r, 3e6, [60e9] * n)
+            assert got == pytest.approx([s * 3e6 / 60e9 for s in range(1, n)], rel=1e-13)
+            # d sub-collectives run back to back: the same last arrival
+            got4 = O.ring_arrival_times(n, r, 3e6 / 4, [60e9] * n, d=4)
+            assert got4 == pytest.approx([t * 3e6 / 4 / 60e9 for t in range(1, 4 * (n - 1) + 1)], rel=1e-13)
+
+
+def test_hop_ring_by_hand_n4():
+    # hops 0->1, 1->2, 2->3 take 1 unit, hop 3->0 takes 4. Rank 0, right after
+    # the slow hop, gets a chunk every 4 units; rank 3, furthest downstream,
+    # gets its first three over fast hops.
+    hops = [1.0, 1.0, 1.0, 0.25]
+    want = {0: [4, 8, 12], 1: [1, 5, 9], 2: [1, 2, 6], 3: [1, 2, 3]}
+    for r, w in want.items():
+        assert O.ring_arrival_times(4, r, 1.0, hops) == pytest.approx(w, abs=1e-15)
+
+
+def test_hop_ring_matches_event_simulation():
+    rng = random.Random(17)
+    for _ in range(150):
+        n = rng.choice([1, 2, 3, 4, 5, 8, 12])
+        hops = [rng.uniform(1e9, 100e9) for _ in range(n)]
+        sim = O.simulate_timed_ring_allgather(n, 2e6, hops)
+        for r in range(n):
+            got = O.ring_arrival_times(n, r, 2e6, hops)
+            assert [c for _, c in sim[r]] == O.schedule("ag", "single", n, r)[1:]
+            assert got == pytest.approx([t for t, _ in sim[r]], rel=1e-13)
+
+
+def test_cross_numa_ring_reaches_8_over_7_of_the_slow_link():
+    # Section III-A, Fig. 5(a): 8 ranks, only hops 3->4 and 7->0 cross the
+    # NUMA boundary (rate B); whatever the faster hops run at, the last
+    # arrival anywhere is 7 chunks over B, an effective (8/7) B, and the
+    # ranks right after the slow hops finish last
+    rng = random.Random(19)
+    B, m = 20e9, 4e6
+    for _ in range(40):
+        hops = [rng.uniform(B, 20 * B) for _ in range(8)]
+        hops[3] = hops[7] = B
+        last = [O.ring_arrival_times(8, r, m, hops)[-1] for r in range(8)]
+        assert max(last) == pytest.approx(7 * m / B, rel=1e-13)
+        assert last[0] == pytest.approx(7 * m / B, rel=1e-13) and last[4] == pytest.approx(7 * m / B, rel=1e-13)
+        assert 8 * m / max(last) == pytest.approx(8 / 7 * B, rel=1e-13)
+
+
+def test_hop_ring_busiest_hop_bounds_the_collective():
+    # every hop carries d (n-1) pieces of m/d one after another, so the rank
+    # after the slowest hop cannot finish before (n-1) m / B_min; arrivals at
+    # a rank are in order
+    rng = random.Random(23)
+    for _ in range(60):
+        n = rng.choice([2, 4, 8])
+        hops = [rng.uniform(1e9, 100e9) for _ in range(n)]
+        slow = min(range(n), key=lambda q: hops[q])
+        for d in (1, 2, 4, 8):
+            t = O.ring_arrival_times(n, (slow + 1) % n, 8e6 / d, hops, d=d)
+            assert t[-1] >= (n - 1) * 8e6 / hops[slow] * (1 - 1e-12)
+            for r in range(n):
+                a = O.ring_arrival_times(n, r, 8e6 / d, hops, d=d)
+                assert all(x < y for x, y in zip(a, a[1:]))

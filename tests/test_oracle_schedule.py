@@ -79,3 +79,15 @@ def test_rs_local_chunk_only_completes_at_owner():
     result, _ = O.simulate_ring_reduce_scatter(partials, "single")
     for q in range(n):
         assert np.all(result[q] == 10.0)
+
+
+@pytest.mark.parametrize("n", [2, 4, 6, 8, 16])
+def test_alltoall_schedule_own_domain_first(n):
+    # own chunk, then every chunk of the own NUMA domain (direct links), then
+    # every chunk of the other domain (shared cross-domain link)
+    h = n // 2
+    for r in range(n):
+        s = O.schedule("ag", "alltoall", n, r)
+        assert sorted(s) == list(range(n)) and s[0] == r
+        assert {q // h for q in s[1:h]} <= {r // h}
+        assert {q // h for q in s[h:]} == {1 - r // h}
