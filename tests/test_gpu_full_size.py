@@ -182,3 +182,20 @@ def test_config5_proportional_double_ring_4_to_1_full_size(pattern):
         C.compass_gemm_rs(case.problem, LINKS_4_TO_1)
         C.compass_sync()
         check_rs(case, inp, 2 * inp["n"], seed=512, extra_rows=split_boundary_rows(inp, 0.2))
+
+
+@pytest.mark.parametrize("ring", ["alltoall", "single_hops"])
+def test_config2_cross_numa_links_full_size(ring):
+    # the fc1 workload over the cross-NUMA link patterns: AlltoAll (own
+    # domain 200 GB/s, 50 GB/s shared across) and the single ring with hops
+    # 3 -> 4 and 7 -> 0 at 50 GB/s, the rest at 200 GB/s (rank 3)
+    inp = inputs(2)
+    _say("config 2 cross-NUMA:", ring)
+    if ring == "alltoall":
+        case, lk = AGCase(inp, 0, "alltoall"), C.links(200e9, 50e9)
+    else:
+        hops = [50e9 if q in (3, 7) else 200e9 for q in range(inp["n"])]
+        case, lk = AGCase(inp, 3, "single"), C.links(200e9, hop_Bps=hops)
+    C.compass_ag_gemm(case.problem, lk)
+    C.compass_sync()
+    check_ag(case, inp, inp["n"], seed=521)

@@ -681,3 +681,42 @@ def test_hop_ring_transfer_follows_the_per_rank_arrival_times():
         assert t[r] < 1.25 * want + 1e-3
         assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
     assert t[3] < 0.8 * t[0]
+
+
+@pytest.mark.parametrize("ring", ["alltoall", "single_hops"])
+def test_ag_gemm_ragged_multi_tile_pinned_sources_numa_links(ring):
+    # several row tiles per chunk, a ragged N and K, remote shards in pinned
+    # host memory, over the two cross-NUMA link patterns
+    n = 4
+    M, N, K = 2048, 776, 1032
+    inp = make_ag_inputs(M, N, K, n, seed=131)
+    if ring == "alltoall":
+        case, lk = AGCase(inp, 2, "alltoall", pinned_remote=True, local_in_place=False), C.links(50e9, 20e9)
+    else:
+        case = AGCase(inp, 2, "single", pinned_remote=True, local_in_place=False)
+        lk = C.links(50e9, hop_Bps=_cross_numa_hops(n, 20e9, 50e9))
+    _say("ag ragged pinned", ring)
+    C.compass_ag_gemm(case.problem, lk)
+    C.compass_sync()
+    assert rel_err(host_f64(case.C), case.reference()) < TOL
+    assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+
+
+@pytest.mark.parametrize("d", [2, 4])
+def test_decomp_rs_hop_ring_integer_exact(d):
+    n = 8
+    M, N, K = 128 * n, 136, 256
+    inp = make_int_rs_inputs(M, N, K, n, seed=140 + d)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    lk = C.links(100e9, hop_Bps=_cross_numa_hops(n, 10e9, 100e9))
+    prow = M // n
+    for r in (0, 3):
+        _say("rs decomp hop ring", d, r)
+        case = RSCase(inp, r, "single")
+        C.compass_decomp_gemm(case.problem, d, lk)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+        for q, snd in enumerate(case.send):
+            if snd is not None:
+                assert np.array_equal(host_bits(snd), ref[q * prow:(q + 1) * prow]), (r, q)
