@@ -102,7 +102,11 @@ extern "C" {
  *                   double ring the forward-ring partition precedes the
  *                   backward-ring one within a step.
  *   ReduceScatter:  textbook ring order (r-1-s) mod n, local chunk last.
- * `out` receives `cap` >= n (single) or 2n (double) int32 entries.
+ *   COMPASS_RING_ALLTOALL (AllGather, even n): chunk ids in the order given
+ *                   with the constant; other patterns or an odd n return
+ *                   COMPASS_ERR_UNSUPPORTED / COMPASS_ERR_INVALID.
+ * `out` receives `cap` >= n (single ring, AlltoAll) or 2n (double ring)
+ * int32 entries.
  * Returns the number of entries written, or a negative status.
  * Host only; needs no GPU. */
 int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int cap);
@@ -136,14 +140,37 @@ int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int c
  * incoming items take the rate of the hop into this rank, the ReduceScatter
  * sums sent onward that of the hop out of it. The caller owns the array; it
  * is read during the call only. Another ring with hop_Bps set returns
- * COMPASS_ERR_UNSUPPORTED. */
+ * COMPASS_ERR_UNSUPPORTED.
+ *
+ * sub_chunks (0 or 1: one arrival flag per partition): s >= 2 splits every
+ * partition's rows into s pieces of consecutive rows (piece t: rows
+ * [cnt t / s, cnt (t+1) / s) of the partition's cnt rows), each moved as an
+ * item of its own, in row order, with an arrival flag of its own, so tiles
+ * start on the first piece before the rest of the partition lands, and
+ * under ReduceScatter each piece's sum is sent on as soon as its tiles are
+ * done. Fused operators, transfer and unfused baseline; needs the single or
+ * double ring without hop_Bps, s times the partition count at most 64, and
+ * a row for every piece (else COMPASS_ERR_UNSUPPORTED / _INVALID);
+ * compass_decomp_gemm with d > 1 returns COMPASS_ERR_UNSUPPORTED. */
 typedef struct compass_links {
     double fwd_Bps;
     double bwd_Bps;
     size_t slice_bytes;
     int    engines_per_ring;
+    int    sub_chunks;
     const double *hop_Bps;
 } compass_links;
+
+/* Partition layout of rank `rank` (host only, no GPU): the P partitions the
+ * operators move and gate on (n or 2n base partitions times sub_chunks),
+ * from pattern, ring, n, M and the link parameters that shape it (the rate
+ * split of COMPASS_RING_DOUBLE_SPLIT, sub_chunks). order[i] is the partition
+ * at schedule position i (each base partition's pieces in row order);
+ * partition q holds global rows [row0[q], row0[q] + rows[q]) for InterDecom
+ * degree 1. Returns P, or a negative status (the operators' checks on
+ * these arguments, a NULL pointer, cap < P). */
+int compass_partition_layout(int pattern, int ring, int n, int rank, int M, const compass_links *l,
+                             int32_t *order, int32_t *row0, int32_t *rows, int cap);
 
 /* ---- one operator instance ----------------------------------------------
  * Describes the rank-local share of one AllGather+GEMM or GEMM+ReduceScatter.

@@ -239,6 +239,66 @@ def schedule(pattern: str, ring: str, n: int, r: int) -> list:
     return out
 
 
+def backward_rows(rows: int, fwd_Bps: float, bwd_Bps: float, ring: str) -> int:
+    """Rows of a chunk (or of an InterDecom piece of one) that the backward
+    ring carries. The paper's double ring splits every chunk in two halves
+    (Section III-B). Reading for the rate-proportional extension
+    (DOUBLE_SPLIT, both rates paced): the backward share is the rate share
+    B_bwd / (B_fwd + B_bwd) of the rows, moved to a multiple of G rows
+    (G = 128, the smaller tile's height, when the block has at least 1024
+    rows, else 8) and kept within [lo, rows - lo], lo = min(G, rows // 2).
+    Of the two nearest such multiples, the one whose step
+    max(h / f_bwd, (rows - h) / f_fwd) is shorter wins; a tie goes to the
+    smaller."""
+    if ring != DOUBLE_SPLIT or not (fwd_Bps > 0 and bwd_Bps > 0):
+        return rows // 2
+    fb = bwd_Bps / (fwd_Bps + bwd_Bps)
+    G = 128 if rows >= 1024 else 8
+    lo = min(G, rows // 2)
+
+    def clamp(h):
+        return min(max(h, lo), rows - lo)
+
+    down = clamp(math.floor(rows * fb / G) * G)
+    up = clamp(math.ceil(rows * fb / G) * G)
+
+    def step(h):
+        return max(h / fb, (rows - h) / (1.0 - fb))
+
+    return up if step(up) < step(down) else down
+
+
+def partition_layout(pattern: str, ring: str, n: int, r: int, M: int, fwd_Bps: float = 0.0,
+                     bwd_Bps: float = 0.0, sub: int = 1):
+    """The partitions rank r moves and gates on: (order, row0, rows).
+
+    Base partitions: chunk c (single ring, AlltoAll), or its backward part
+    2c and forward part 2c + 1 (double ring, Section III-B), in the order of
+    ``schedule``. With sub-chunk flags (sub >= 2) every base partition's
+    cnt rows are cut into sub pieces of consecutive rows, piece t holding
+    rows [cnt t // sub, cnt (t+1) // sub) of it; partition b * sub + t is
+    piece t of base partition b and the pieces of a base partition follow
+    one another in the order. Returns the order and, per partition id, its
+    first global row and row count."""
+    rows = M // n
+    two = ring in (DOUBLE, DOUBLE_SPLIT)
+    base = []
+    for c in range(n):
+        if two:
+            h0 = backward_rows(rows, fwd_Bps, bwd_Bps, ring)
+            base += [(c * rows, h0), (c * rows + h0, rows - h0)]
+        else:
+            base.append((c * rows, rows))
+    row0, cnt = [], []
+    for start, size in base:
+        for t in range(sub):
+            lo, hi = size * t // sub, size * (t + 1) // sub
+            row0.append(start + lo)
+            cnt.append(hi - lo)
+    order = [b * sub + t for b in schedule(pattern, ring, n, r) for t in range(sub)]
+    return order, row0, cnt
+
+
 def simulate_ring_allgather(n: int, ring: str) -> list:
     """Message-passing simulation of a ring AllGather over n ranks.
 

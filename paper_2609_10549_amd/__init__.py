@@ -17,6 +17,7 @@ from .compass import (  # noqa: F401
     compass_probe_mfma,
     compass_last_error,
     compass_model_t_comm,
+    compass_partition_layout,
     compass_ring_arrival_times,
     compass_model_t_decomp,
     compass_model_t_fusion,

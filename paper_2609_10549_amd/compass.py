@@ -53,7 +53,7 @@ class CompassError(RuntimeError):
 class compass_links(ctypes.Structure):
     _fields_ = [("fwd_Bps", ctypes.c_double), ("bwd_Bps", ctypes.c_double),
                 ("slice_bytes", ctypes.c_size_t), ("engines_per_ring", ctypes.c_int),
-                ("hop_Bps", ctypes.POINTER(ctypes.c_double))]
+                ("sub_chunks", ctypes.c_int), ("hop_Bps", ctypes.POINTER(ctypes.c_double))]
 
 
 class compass_problem(ctypes.Structure):
@@ -116,6 +116,10 @@ _SIGS = {
     "compass_set_option": (ctypes.c_int, [ctypes.c_int, ctypes.c_longlong]),
     "compass_pick_strategy": (ctypes.c_int, [ctypes.POINTER(compass_workload), ctypes.POINTER(compass_topology),
                                              ctypes.POINTER(compass_calib), ctypes.POINTER(compass_choice)]),
+    "compass_partition_layout": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                ctypes.POINTER(compass_links), ctypes.POINTER(ctypes.c_int32),
+                                                ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                                ctypes.c_int]),
     "compass_ring_arrival_times": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_double,
                                                   ctypes.POINTER(ctypes.c_double), ctypes.c_int,
                                                   ctypes.POINTER(ctypes.c_double), ctypes.c_int]),
@@ -217,9 +221,10 @@ def rs_problem(A, W, partial_src: Sequence, partial_stage, C, send_dst: Sequence
 
 
 def links(fwd_Bps: float = 0.0, bwd_Bps: float | None = None, slice_bytes: int = 0,
-          engines_per_ring: int = 0, hop_Bps: Sequence[float] | None = None) -> compass_links:
+          engines_per_ring: int = 0, hop_Bps: Sequence[float] | None = None,
+          sub_chunks: int = 0) -> compass_links:
     lk = compass_links(fwd_Bps=fwd_Bps, bwd_Bps=fwd_Bps if bwd_Bps is None else bwd_Bps,
-                       slice_bytes=slice_bytes, engines_per_ring=engines_per_ring)
+                       slice_bytes=slice_bytes, engines_per_ring=engines_per_ring, sub_chunks=sub_chunks)
     if hop_Bps is not None:
         arr = (ctypes.c_double * len(hop_Bps))(*hop_Bps)
         lk.hop_Bps = arr
@@ -305,6 +310,16 @@ def compass_pick_strategy(workload: compass_workload, topology: compass_topology
     _check(lib().compass_pick_strategy(ctypes.byref(workload), ctypes.byref(topology), ctypes.byref(calib),
                                        ctypes.byref(out)), "compass_pick_strategy")
     return out
+
+
+def compass_partition_layout(pattern, ring, n: int, rank: int, M: int, lk: compass_links | None = None):
+    """(order, row0, rows) of the partitions of one rank; see the header."""
+    cap = 64
+    order, row0, rows = (ctypes.c_int32 * cap)(), (ctypes.c_int32 * cap)(), (ctypes.c_int32 * cap)()
+    k = _check(lib().compass_partition_layout(PATTERNS.get(pattern, pattern), RINGS.get(ring, ring), n, rank, M,
+                                              ctypes.byref(_lk(lk)), order, row0, rows, cap),
+               "compass_partition_layout")
+    return list(order[:k]), list(row0[:k]), list(rows[:k])
 
 
 def compass_ring_arrival_times(n: int, rank: int, piece_bytes: float, hop_Bps: Sequence[float],

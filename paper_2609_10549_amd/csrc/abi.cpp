@@ -51,6 +51,11 @@ int compass_pick_strategy(const compass_workload *w, const compass_topology *t, 
     return pick(w, t, cal, out);
 }
 
+int compass_partition_layout(int pattern, int ring, int n, int rank, int M, const compass_links *l, int32_t *order,
+                             int32_t *row0, int32_t *rows, int cap) {
+    return op_partition_layout(pattern, ring, n, rank, M, l, order, row0, rows, cap);
+}
+
 int compass_ring_arrival_times(int n, int rank, double piece_bytes, const double *hop_Bps, int d, double *out,
                                int cap) {
     return ring_arrivals(n, rank, piece_bytes, hop_Bps, d, out, cap);

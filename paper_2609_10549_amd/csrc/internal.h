@@ -25,6 +25,8 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream);
 int op_decomp(const compass_problem *p, int d, const compass_links *l, void *stream);
 int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream);
 int op_transfer(const compass_problem *p, const compass_links *l, void *stream);
+int op_partition_layout(int pattern, int ring, int n, int rank, int M, const compass_links *l, int32_t *order,
+                        int32_t *row0, int32_t *rows, int cap);
 int op_sequential(const compass_problem *p, const compass_links *l, void *stream);
 int op_sync();
 int op_set_option(int key, long long value);

@@ -668,10 +668,17 @@ static inline bool two_rings(const compass_problem *p) {
     return p->ring == COMPASS_RING_DOUBLE || p->ring == COMPASS_RING_DOUBLE_SPLIT;
 }
 
+// Partitions: the ring's base partitions (a chunk, or a chunk's part on one
+// ring of the double ring), each split into `sub` pieces of consecutive rows
+// with a copy and an arrival flag of their own (sub-chunk flags). Partition
+// q is piece q % sub of base partition q / sub, so partition ids still grow
+// with the row.
 struct Geometry {
-    int P;           // partitions
+    int P;           // partitions, BP * sub
+    int BP;          // base partitions: n (single ring) or 2n (double ring)
+    int sub;         // pieces per base partition (1: one flag per base partition)
     int rows;        // rows per chunk
-    int prow;        // rows per partition (double ring: half a chunk)
+    int prow;        // rows per base partition (double ring: half a chunk)
     bool dbl;        // double ring (either split)
     double fb;       // double ring: share of a chunk's rows on the backward ring
     int32_t sched[2 * kMaxRanks];
@@ -696,37 +703,97 @@ static int half0(const Geometry &g, int r) {
     return step(up) < step(dn) ? up : dn;
 }
 
+// Rows [*off, *off + *cnt) of a block of r chunk rows that base partition
+// half h carries (single ring: all of them).
+static void base_rows(const Geometry &g, int r, int h, int *off, int *cnt) {
+    if (!g.dbl) { *off = 0; *cnt = r; return; }
+    const int h0 = half0(g, r);
+    *off = h ? h0 : 0;
+    *cnt = h ? r - h0 : h0;
+}
+
+// Piece t of `sub` of a base block of cnt rows: rows [cnt t / sub, cnt (t+1) / sub).
+static inline int piece_lo(int cnt, int t, int sub) { return (int)((long)cnt * t / sub); }
+
 // Partition holding global row r (the fused operators' arrival gates).
 static int part_of_row(const Geometry &g, int r) {
     const int c = r / g.rows;
-    if (!g.dbl) return c;
-    return 2 * c + ((r - c * g.rows) < half0(g, g.rows) ? 0 : 1);
+    const int in = r - c * g.rows;
+    int h = 0;
+    if (g.dbl) h = in < half0(g, g.rows) ? 0 : 1;
+    const int b = g.dbl ? 2 * c + h : c;
+    if (g.sub == 1) return b;
+    int off, cnt;
+    base_rows(g, g.rows, h, &off, &cnt);
+    int t = g.sub - 1;
+    while (t > 0 && piece_lo(cnt, t, g.sub) > in - off) --t;
+    return b * g.sub + t;
 }
 
 // Rows of the smallest partition.
 static int min_part_rows(const Geometry &g) {
-    if (!g.dbl) return g.rows;
-    const int h0 = half0(g, g.rows);
-    return std::min(h0, g.rows - h0);
+    int m = g.rows;
+    if (g.dbl) {
+        const int h0 = half0(g, g.rows);
+        m = std::min(h0, g.rows - h0);
+    }
+    return m / g.sub;
+}
+
+// The partition layout of one rank: pattern, ring, ranks, rows and the link
+// parameters that shape it (the rate split of COMPASS_RING_DOUBLE_SPLIT,
+// sub-chunk flags). Host only.
+static int make_geometry(int pattern, int ring, int n, int rank, int M, const compass_links *l, Geometry *g) {
+    if (pattern != COMPASS_AG_GEMM && pattern != COMPASS_GEMM_RS) return set_error(COMPASS_ERR_INVALID, "unknown pattern");
+    if (ring != COMPASS_RING_SINGLE && ring != COMPASS_RING_DOUBLE && ring != COMPASS_RING_DOUBLE_SPLIT &&
+        ring != COMPASS_RING_ALLTOALL)
+        return set_error(COMPASS_ERR_INVALID, "unknown ring");
+    if (n < 1 || n > kMaxRanks || rank < 0 || rank >= n)
+        return set_error(COMPASS_ERR_INVALID, "need 1 <= n <= %d and 0 <= rank < n", kMaxRanks);
+    if (ring == COMPASS_RING_ALLTOALL) {
+        if (pattern != COMPASS_AG_GEMM) return set_error(COMPASS_ERR_UNSUPPORTED, "the AlltoAll pattern is AllGather only");
+        if (n % 2) return set_error(COMPASS_ERR_INVALID, "the AlltoAll pattern needs an even n");
+    }
+    if (M < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
+    const bool dbl = ring == COMPASS_RING_DOUBLE || ring == COMPASS_RING_DOUBLE_SPLIT;
+    const int BP = dbl ? 2 * n : n;
+    if (l->sub_chunks < 0) return set_error(COMPASS_ERR_INVALID, "sub_chunks < 0");
+    const int sub = l->sub_chunks > 1 ? l->sub_chunks : 1;
+    if (sub > 1) {
+        if (l->hop_Bps || ring == COMPASS_RING_ALLTOALL)
+            return set_error(COMPASS_ERR_UNSUPPORTED, "sub-chunk flags need the single or double ring with uniform hops");
+        if ((long)BP * sub > 2 * kMaxRanks)
+            return set_error(COMPASS_ERR_UNSUPPORTED, "partitions x sub-chunks above %d", 2 * kMaxRanks);
+    }
+    if (M % BP) return set_error(COMPASS_ERR_INVALID, "M must be divisible by %d", BP);
+    g->P = BP * sub;
+    g->BP = BP;
+    g->sub = sub;
+    g->rows = M / n;
+    g->prow = M / BP;
+    g->dbl = dbl;
+    g->fb = 0.5;
+    if (ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0)
+        g->fb = l->bwd_Bps / (l->fwd_Bps + l->bwd_Bps);
+    if (min_part_rows(*g) < 1)
+        return set_error(COMPASS_ERR_INVALID, "sub_chunks %d leaves a partition without rows", sub);
+    int32_t base[2 * kMaxRanks];
+    const int len = schedule_fill(pattern, ring, n, rank, base, 2 * kMaxRanks);
+    if (len != BP) return len < 0 ? len : set_error(COMPASS_ERR_INVALID, "schedule failed");
+    // each base partition's pieces in row order
+    for (int i = 0; i < BP; ++i)
+        for (int t = 0; t < sub; ++t) g->sched[i * sub + t] = base[i] * sub + t;
+    for (int i = 0; i < g->P; ++i) g->pos[g->sched[i]] = i;
+    return COMPASS_OK;
 }
 
 static int validate(const compass_problem *p, const compass_links *l, int want_pattern, Geometry *g) {
     if (!p) return set_error(COMPASS_ERR_INVALID, "problem is NULL");
     if (!l) return set_error(COMPASS_ERR_INVALID, "links is NULL");
     if (want_pattern >= 0 && p->pattern != want_pattern) return set_error(COMPASS_ERR_INVALID, "wrong pattern for this call");
-    if (p->pattern != COMPASS_AG_GEMM && p->pattern != COMPASS_GEMM_RS) return set_error(COMPASS_ERR_INVALID, "unknown pattern");
-    if (p->ring != COMPASS_RING_SINGLE && p->ring != COMPASS_RING_DOUBLE && p->ring != COMPASS_RING_DOUBLE_SPLIT &&
-        p->ring != COMPASS_RING_ALLTOALL)
-        return set_error(COMPASS_ERR_INVALID, "unknown ring");
-    if (p->n < 1 || p->n > kMaxRanks || p->rank < 0 || p->rank >= p->n)
-        return set_error(COMPASS_ERR_INVALID, "need 1 <= n <= %d and 0 <= rank < n", kMaxRanks);
-    if (p->ring == COMPASS_RING_ALLTOALL) {
-        if (p->pattern != COMPASS_AG_GEMM) return set_error(COMPASS_ERR_UNSUPPORTED, "the AlltoAll pattern is AllGather only");
-        if (p->n % 2) return set_error(COMPASS_ERR_INVALID, "the AlltoAll pattern needs an even n");
-    }
-    if (p->M < 1 || p->N < 1 || p->K < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
-    const int P = two_rings(p) ? 2 * p->n : p->n;
-    if (p->M % P) return set_error(COMPASS_ERR_INVALID, "M must be divisible by %d", P);
+    int rc = make_geometry(p->pattern, p->ring, p->n, p->rank, p->M, l, g);
+    if (rc != COMPASS_OK) return rc;
+    if (p->N < 1 || p->K < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
     if (p->K % 8 || p->N % 8) return set_error(COMPASS_ERR_INVALID, "K and N must be multiples of 8");
     if ((p->M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
     if ((double)p->M * p->K * 2 > 1073741824.0 || (double)p->N * p->K * 2 > 1073741824.0 ||
@@ -756,16 +823,6 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
             if (!std::isfinite(l->hop_Bps[q]) || l->hop_Bps[q] < 1e8)
                 return set_error(COMPASS_ERR_INVALID, "hop %d: per-hop rates must be at least 1e8 bytes/s", q);
     }
-    g->P = P;
-    g->rows = p->M / p->n;
-    g->prow = p->M / P;
-    g->dbl = two_rings(p);
-    g->fb = 0.5;
-    if (p->ring == COMPASS_RING_DOUBLE_SPLIT && l->fwd_Bps > 0 && l->bwd_Bps > 0)
-        g->fb = l->bwd_Bps / (l->fwd_Bps + l->bwd_Bps);
-    const int len = schedule_fill(p->pattern, p->ring, p->n, p->rank, g->sched, 2 * kMaxRanks);
-    if (len != P) return len < 0 ? len : set_error(COMPASS_ERR_INVALID, "schedule failed");
-    for (int i = 0; i < P; ++i) g->pos[g->sched[i]] = i;
     return COMPASS_OK;
 }
 
@@ -940,16 +997,36 @@ static hipError_t copy_if_needed(void *dst, const void *src, size_t bytes, hipSt
     return hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, s);
 }
 
-// Partition p's rows (identity map): chunk c = p (single) or p / 2 (double).
-static inline int part_chunk(const compass_problem *p, int q) { return two_rings(p) ? q / 2 : q; }
-static inline int part_half(const compass_problem *p, int q) { return two_rings(p) ? q % 2 : 0; }
-static inline bool part_fwd(const compass_problem *p, int q) { return !two_rings(p) || (q % 2) == 1; }
-// Rows [*off, *off + *cnt) of a block of r chunk rows that partition half h carries.
-static inline void part_rows(const compass_problem *p, const Geometry &g, int r, int h, int *off, int *cnt) {
-    if (!two_rings(p)) { *off = 0; *cnt = r; return; }
-    const int h0 = half0(g, r);
-    *off = h ? h0 : 0;
-    *cnt = h ? r - h0 : h0;
+// Partition q's rows (identity map): base partition b = q / sub; chunk
+// c = b (single ring) or b / 2 (double ring).
+static inline int part_chunk(const Geometry &g, int q) { return g.dbl ? q / g.sub / 2 : q / g.sub; }
+static inline int part_half(const Geometry &g, int q) { return g.dbl ? (q / g.sub) % 2 : 0; }
+static inline bool part_fwd(const Geometry &g, int q) { return !g.dbl || (q / g.sub) % 2 == 1; }
+// Rows [*off, *off + *cnt) of a block of r chunk rows that partition q carries.
+static inline void part_rows(const Geometry &g, int r, int q, int *off, int *cnt) {
+    int bo, bc;
+    base_rows(g, r, part_half(g, q), &bo, &bc);
+    const int t = q % g.sub;
+    const int lo = piece_lo(bc, t, g.sub), hi = piece_lo(bc, t + 1, g.sub);
+    *off = bo + lo;
+    *cnt = hi - lo;
+}
+
+int op_partition_layout(int pattern, int ring, int n, int rank, int M, const compass_links *l, int32_t *order,
+                        int32_t *row0, int32_t *rows, int cap) {
+    if (!l || !order || !row0 || !rows) return set_error(COMPASS_ERR_INVALID, "partition_layout: NULL argument");
+    Geometry g;
+    const int rc = make_geometry(pattern, ring, n, rank, M, l, &g);
+    if (rc != COMPASS_OK) return rc;
+    if (cap < g.P) return set_error(COMPASS_ERR_INVALID, "partition_layout: cap below %d", g.P);
+    for (int q = 0; q < g.P; ++q) {
+        order[q] = g.sched[q];
+        int off, cnt;
+        part_rows(g, g.rows, q, &off, &cnt);
+        row0[q] = part_chunk(g, q) * g.rows + off;
+        rows[q] = cnt;
+    }
+    return g.P;
 }
 
 static int make_item(Item *it, void *dst, const void *src, size_t bytes, int flag, int gate) {
@@ -1014,11 +1091,11 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
     for (int j = 0; j < d; ++j) {
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
-            const int c = part_chunk(p, q), h = part_half(p, q);
+            const int c = part_chunk(geo, q);
             if (c == p->rank) continue;
             if (q == g_ctx.drop_flag && d == 1) continue;
             int off, piece;                                          // rows of this item
-            part_rows(p, geo, pc, h, &off, &piece);
+            part_rows(geo, pc, q, &off, &piece);
             const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
@@ -1027,7 +1104,7 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
             if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s
-            const bool on_fwd = a2a ? (c / dom == p->rank / dom) : part_fwd(p, q);
+            const bool on_fwd = a2a ? (c / dom == p->rank / dom) : part_fwd(geo, q);
             (on_fwd ? fwd : bwd)->items.push_back(it);
         }
     }
@@ -1065,9 +1142,9 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
             if (resident & (1ull << q)) continue;
-            const int c = part_chunk(p, q), h = part_half(p, q);
+            const int c = part_chunk(geo, q);
             int off, piece;
-            part_rows(p, geo, pc, h, &off, &piece);
+            part_rows(geo, pc, q, &off, &piece);
             const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
@@ -1076,15 +1153,15 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
             if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s >= 1
-            jobs[part_fwd(p, q) ? 0 : 1].items.push_back(it);
+            jobs[part_fwd(geo, q) ? 0 : 1].items.push_back(it);
         }
         if (!p->send_dst) continue;
         for (int s = 0; s < geo.P; ++s) {
             const int q = geo.sched[s];
-            const int c = part_chunk(p, q), h = part_half(p, q);
+            const int c = part_chunk(geo, q);
             if (c == p->rank) continue;
             int off, piece;
-            part_rows(p, geo, pc, h, &off, &piece);
+            part_rows(geo, pc, q, &off, &piece);
             const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             const size_t row = (size_t)c * geo.rows + row_in_chunk;
             Item it;
@@ -1092,7 +1169,7 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      (const char *)p->C + row * N * 2, (size_t)piece * N * 2, -1,
                                      gate_out ? j * geo.P + q : -1);
             if (rc != COMPASS_OK) return rc;
-            jobs[part_fwd(p, q) ? 2 : 3].items.push_back(it);
+            jobs[part_fwd(geo, q) ? 2 : 3].items.push_back(it);
         }
     }
     for (int r = 2; r < 4; ++r)
@@ -1100,19 +1177,25 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
     return COMPASS_OK;
 }
 
+// Partitions in place before the operator starts: the rank's own chunk
+// (AllGather), or the first step's partials (ReduceScatter), all their pieces.
 static uint64_t resident_mask(const compass_problem *p, const Geometry &geo) {
-    if (p->pattern == COMPASS_AG_GEMM) {
-        if (!two_rings(p)) return 1ull << p->rank;
-        return 3ull << (2 * p->rank);
-    }
-    if (!two_rings(p)) return 1ull << geo.sched[0];
-    return (1ull << geo.sched[0]) | (1ull << geo.sched[1]);
+    uint64_t base = 0;
+    if (p->pattern == COMPASS_AG_GEMM)
+        base = geo.dbl ? 3ull << (2 * p->rank) : 1ull << p->rank;
+    else
+        base = geo.dbl ? (1ull << (geo.sched[0] / geo.sub)) | (1ull << (geo.sched[geo.sub] / geo.sub))
+                       : 1ull << (geo.sched[0] / geo.sub);
+    uint64_t m = 0;
+    for (int q = 0; q < geo.P; ++q)
+        if (base & (1ull << (q / geo.sub))) m |= 1ull << q;
+    return m;
 }
 
 static uint64_t nonlocal_mask(const compass_problem *p, const Geometry &geo) {
     uint64_t m = 0;
     for (int q = 0; q < geo.P; ++q)
-        if (part_chunk(p, q) != p->rank) m |= 1ull << q;
+        if (part_chunk(geo, q) != p->rank) m |= 1ull << q;
     return m;
 }
 
@@ -1131,9 +1214,9 @@ static int stage_resident_partials(const compass_problem *p, const Geometry &geo
     const int pc = geo.rows / d;
     for (int q = 0; q < geo.P; ++q) {
         if (!(resident & (1ull << q))) continue;
-        const int c = part_chunk(p, q), h = part_half(p, q);
+        const int c = part_chunk(geo, q);
         int off, cnt;
-        part_rows(p, geo, pc, h, &off, &cnt);
+        part_rows(geo, pc, q, &off, &cnt);
         for (int j = 0; j < d; ++j) {
             const size_t row_in_chunk = (size_t)j * pc + (size_t)off;
             void *dst = (char *)p->partial_stage + ((size_t)c * geo.rows + row_in_chunk) * N * 4;
@@ -1268,7 +1351,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     init_params(g, epoch);
     // (rate-proportional parts: a 256-row tile may span both parts of a
     // chunk and waits for the later one, which an AllGather tolerates)
-    const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 ? geo.rows : min_part_rows(geo),
+    const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 && geo.sub == 1 ? geo.rows : min_part_rows(geo),
                               lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
     order_by_schedule(g, cfg, geo, p->M, true);
@@ -1329,6 +1412,8 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
         return set_error(COMPASS_ERR_INVALID, "d must be a power of two dividing %d", geo.prow);
     if (d > 1 && p->ring == COMPASS_RING_ALLTOALL)
         return set_error(COMPASS_ERR_UNSUPPORTED, "InterDecom runs over the rings only");
+    if (d > 1 && geo.sub > 1)
+        return set_error(COMPASS_ERR_UNSUPPORTED, "InterDecom takes one flag per piece (sub_chunks <= 1)");
     if (d * geo.P > kFinalFlag0) return set_error(COMPASS_ERR_UNSUPPORTED, "d * partitions exceeds the flag slots");
     if ((rc = begin()) != COMPASS_OK) return rc;
     hipStream_t s = (hipStream_t)stream;

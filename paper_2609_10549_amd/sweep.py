@@ -25,6 +25,8 @@
   AlltoAll pattern (own-domain links at 200 GB/s, all cross-domain flows
   sharing B): transfer alone, fused and unfused, their effective bandwidths
   and the model's T_comm.
+* Sub-chunk arrival flags: the benchmark's two operators and the GPT-3
+  AllGather with 1, 2, 4 (and 8) arrival flags per partition.
 * torch.matmul (hipBLASLt) on every GEMM shape, for context.
 
 Timing only: the inputs are seeded random bf16 on the GPU (parity is the
@@ -240,7 +242,38 @@ def numa_study(verbose):
     return res
 
 
-STUDIES = ("decomp", "mlp", "high", "gpt3_ag", "gpt3_rs", "numa")
+SUBCHUNK_CASES = (("ag", 8192, 2048, 4096, "double", 0.0, 0.0), ("ag", 8192, 2048, 4096, "double", 150e9, 150e9),
+                  ("ag", 8192, 2048, 4096, "double", 216e9, 216e9), ("rs", 8192, 4096, 2048, "single", 0.0, 0.0),
+                  ("rs", 8192, 4096, 2048, "single", 150e9, 150e9),
+                  ("ag", 8192, 6144, 12288, "double_split", 257e9, 64e9))
+
+
+def subchunk_study(verbose):
+    """Sub-chunk arrival flags: transfer and fused times of the benchmark's
+    two operators and the GPT-3 AllGather against the number of flags per
+    partition (1, 2, 4, and 8 where the 64-partition limit allows)."""
+    res = []
+    for pat, M, N, K, ring, fwd, bwd in SUBCHUNK_CASES:
+        buf = CAL.Buffers(pat, M, N, K, 8, ring)
+        fns = {"g": lambda: C.compass_gemm(buf.A, buf.W, buf.C, buf.P)}
+        subs = [s for s in (1, 2, 4, 8) if (16 if ring != "single" else 8) * s <= 64]
+        for sub in subs:
+            lk = C.links(fwd, bwd, sub_chunks=sub)
+            fns[("x", sub)] = (lambda lk=lk: C.compass_transfer(buf.problem, lk))
+            fns[("f", sub)] = (lambda lk=lk: _fused(pat)(buf.problem, lk))
+        t = CAL.time_interleaved(fns, reps=7)
+        pt = dict(pattern=pat, M=M, N=N, K=K, ring=ring, fwd_Bps=fwd, bwd_Bps=bwd, t_gemm_us=t["g"] * 1e6,
+                  t_xfer_us={str(s): t[("x", s)] * 1e6 for s in subs},
+                  t_fused_us={str(s): t[("f", s)] * 1e6 for s in subs})
+        res.append(pt)
+        if verbose:
+            print(json.dumps(pt), flush=True)
+        del buf
+        torch.cuda.empty_cache()
+    return res
+
+
+STUDIES = ("decomp", "mlp", "high", "gpt3_ag", "gpt3_rs", "numa", "subchunk")
 
 
 def run_study(name, quick, cal):
@@ -257,6 +290,8 @@ def run_study(name, quick, cal):
             return {}
         return {"high_lambda_ag": lambda_study("ag", 8192, 16384, 4096, 8, "double", high, True),
                 "high_lambda_rs": lambda_study("rs", 8192, 4096, 16384, 8, "single", high, True)}
+    if name == "subchunk":
+        return {"subchunk_flags": subchunk_study(True)}
     if name == "numa":
         return {"numa_single_vs_alltoall": numa_study(True)}
     if name.startswith("gpt3_"):

@@ -96,6 +96,46 @@ def test_ring_arrival_times_match_oracle():
             C.compass_ring_arrival_times(*args)
 
 
+def test_partition_layout_bit_exact_vs_oracle():
+    rng = random.Random(31)
+    checked = 0
+    for _ in range(400):
+        ring = rng.choice(["single", "double", "double_split"])
+        pat = rng.choice(["ag", "rs"])
+        n = rng.choice([1, 2, 3, 4, 8, 16])
+        base = n * (2 if ring != "single" else 1)
+        sub = rng.choice([0, 1, 2, 3, 4, 8])
+        if base * max(sub, 1) > 64:
+            continue
+        M = base * rng.choice([1, 3, 8, 64, 128, 512, 1024, 1536])
+        fwd, bwd = rng.choice([(0.0, 0.0), (200e9, 50e9), (50e9, 200e9), (1e9, 3e9)])
+        r = rng.randrange(n)
+        ref = O.partition_layout(pat, ring, n, r, M, fwd, bwd, max(sub, 1))
+        if min(ref[2]) < 1:
+            with pytest.raises(C.CompassError):
+                C.compass_partition_layout(pat, ring, n, r, M, C.links(fwd, bwd, sub_chunks=sub))
+            continue
+        got = C.compass_partition_layout(pat, ring, n, r, M, C.links(fwd, bwd, sub_chunks=sub))
+        assert got == (ref[0], ref[1], ref[2]), (pat, ring, n, r, M, sub, fwd, bwd)
+        checked += 1
+    assert checked > 250
+
+
+def test_sub_chunk_refusals_before_enqueue():
+    lib = C.lib()
+    for ring, kw, want in ((C.RING_ALLTOALL, dict(sub_chunks=2), C.ERR_UNSUPPORTED),
+                           (C.RING_SINGLE, dict(sub_chunks=2, hop_Bps=[1e9, 1e9]), C.ERR_UNSUPPORTED),
+                           (C.RING_DOUBLE, dict(sub_chunks=17), C.ERR_UNSUPPORTED),   # 4 x 17 > 64
+                           (C.RING_SINGLE, dict(sub_chunks=-1), C.ERR_INVALID),
+                           (C.RING_SINGLE, dict(sub_chunks=16), C.ERR_INVALID)):      # 8 rows, 16 pieces
+        st, keep = _fake_problem(C.AG_GEMM, 16, 64, 64, 2, ring=ring)
+        lk = C.links(1e9, 1e9, **kw)
+        assert lib.compass_ag_gemm(ctypes.byref(st), ctypes.byref(lk), None) == want, (ring, kw)
+    st, keep = _fake_problem(C.GEMM_RS, 64, 64, 64, 2)
+    lk = C.links(1e9, 1e9, sub_chunks=2)
+    assert lib.compass_decomp_gemm(ctypes.byref(st), 2, ctypes.byref(lk), None) == C.ERR_UNSUPPORTED
+
+
 def test_hop_rates_refused_off_the_single_ring_or_out_of_range():
     lib = C.lib()
     for ring in (C.RING_DOUBLE, C.RING_DOUBLE_SPLIT, C.RING_ALLTOALL):

@@ -199,3 +199,24 @@ def test_config2_cross_numa_links_full_size(ring):
     C.compass_ag_gemm(case.problem, lk)
     C.compass_sync()
     check_ag(case, inp, inp["n"], seed=521)
+
+
+@pytest.mark.parametrize("pattern", ["ag", "rs"])
+def test_config2_config3_sub_chunk_flags_full_size(pattern):
+    # the benchmark's two operators with four arrival flags per partition
+    # (128-row pieces for the AllGather's 512-row partitions)
+    lk = C.links(0.0, 0.0, sub_chunks=4)
+    if pattern == "ag":
+        inp = inputs(2)
+        case = AGCase(inp, 0, "double")
+        _say("config 2 sub-chunks")
+        C.compass_ag_gemm(case.problem, lk)
+        C.compass_sync()
+        check_ag(case, inp, 8 * inp["n"], seed=531)
+    else:
+        inp = inputs(3)
+        case = RSCase(inp, 0, "single")
+        _say("config 3 sub-chunks")
+        C.compass_gemm_rs(case.problem, lk)
+        C.compass_sync()
+        check_rs(case, inp, 4 * inp["n"], seed=532)

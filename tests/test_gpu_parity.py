@@ -720,3 +720,72 @@ def test_decomp_rs_hop_ring_integer_exact(d):
         for q, snd in enumerate(case.send):
             if snd is not None:
                 assert np.array_equal(host_bits(snd), ref[q * prow:(q + 1) * prow]), (r, q)
+
+
+# ------------------------------------------------------------ sub-chunk arrival flags
+@pytest.mark.parametrize("ring", ["single", "double", "double_split"])
+@pytest.mark.parametrize("sub", [2, 4])
+def test_ag_gemm_sub_chunks_integer_exact_all_ranks(ring, sub):
+    n = 8
+    M, N, K = 64 * 2 * n, 264, 200
+    inp = make_int_ag_inputs(M, N, K, n, seed=150 + sub)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    for lk in (C.links(200e9, 50e9, sub_chunks=sub), C.links(0.0, 0.0, sub_chunks=sub)):
+        for r in range(n):
+            _say("ag sub-chunks int", ring, sub, r, lk.fwd_Bps)
+            case = AGCase(inp, r, ring)
+            C.compass_ag_gemm(case.problem, lk)
+            C.compass_sync()
+            assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+
+
+@pytest.mark.parametrize("ring", ["single", "double", "double_split"])
+@pytest.mark.parametrize("sub", [2, 4])
+def test_gemm_rs_sub_chunks_integer_exact(ring, sub):
+    n = 8
+    M, N, K = 128 * n, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=160 + sub)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    rows = M // n
+    for lk in (C.links(200e9, 50e9, sub_chunks=sub), C.links(0.0, 0.0, sub_chunks=sub)):
+        for r in (0, 5):
+            _say("rs sub-chunks int", ring, sub, r, lk.fwd_Bps)
+            case = RSCase(inp, r, ring)
+            C.compass_gemm_rs(case.problem, lk)
+            C.compass_sync()
+            assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
+            for q in range(n):
+                if q != r:
+                    assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
+
+
+def test_sub_chunks_sequential_transfer_and_decomp_d1():
+    n = 4
+    inp = make_int_ag_inputs(512, 136, 264, n, seed=171)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    lk = C.links(100e9, 100e9, sub_chunks=4)
+    for call in ("sequential", "decomp1", "transfer"):
+        _say("sub-chunks", call)
+        case = AGCase(inp, 1, "double")
+        if call == "sequential":
+            C.compass_sequential(case.problem, lk)
+        elif call == "decomp1":
+            C.compass_decomp_gemm(case.problem, 1, lk)
+        else:
+            C.compass_transfer(case.problem, lk)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"]))
+        if call != "transfer":
+            assert np.array_equal(host_bits(case.C), ref)
+    rin = make_int_rs_inputs(512, 136, 264, n, seed=172)
+    rref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(rin["A"]), O.bf16_to_f64(rin["W"]),
+                                       [p.astype(np.float64) for p in rin["P_in"]], n))
+    case = RSCase(rin, 2, "single")
+    # the unfused ReduceScatter's epilogue reads the staged partials as they
+    # are at launch: stage them with a transfer first
+    C.compass_transfer(case.problem, lk)
+    C.compass_sync()
+    C.compass_sequential(case.problem, lk)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), rref)
