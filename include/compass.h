@@ -292,6 +292,15 @@ int compass_sync(void);
                                        fewer tiles than half the workgroup slots split K
                                        (fp32 partial tiles in a library workspace of
                                        CUs x 256 KiB, summed in slice order) */
+#define COMPASS_OPT_POOL        10  /* unpaced links with more than one active direction
+                                       (double ring; ReduceScatter incoming and outgoing):
+                                       > 0 = the directions share every copy engine, each
+                                       engine with at most this many copies queued, slices
+                                       taken in transfer order (an outgoing sum right after
+                                       its partition's incoming partial) from items that are
+                                       ready; 0 = the engines split per direction in
+                                       proportion to their bytes (default 2: a queued copy
+                                       hides the copy side's reaction time; at most 8) */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

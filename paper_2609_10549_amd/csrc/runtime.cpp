@@ -9,7 +9,9 @@
 // partition's arrival flag (a release store of the call's epoch into pinned
 // host memory) once all of its slices have landed. Copies never depend on one
 // another through signals: every completion signal is re-armed only after the
-// copy it tracked has completed.
+// copy it tracked has completed. Unpaced operators with several active
+// directions instead run one pooled job on every engine (execute_pooled):
+// the directions then share the engines slice by slice, in transfer order.
 //
 // Operators (Section III-B TA-IntraFusion, Section II-B / IV InterDecom) are
 // built from one persistent GEMM launch (or d launches) plus these jobs. Row
@@ -75,6 +77,7 @@ static double now_s() {
 constexpr int kRoles = 4;            // in-fwd, in-bwd, out-fwd, out-bwd
 constexpr int kSignals = 256;        // completion signals per pacer
 constexpr size_t kDefaultSlice = 2u << 20;
+constexpr int kDefaultPoolDepth = 2;
 constexpr int kSchedFineQueues = 1, kSchedSpread = 2, kSchedSplitK = 4;
 // split-K workspace: one fp32 partial tile per workgroup slot (the largest
 // of 256 x 256 on one workgroup per CU and 128 x 128 on two)
@@ -99,6 +102,7 @@ struct Item {
     int flag;   // arrival flag to publish after the item, -1: none
     int gate;   // host done flag to wait for before the item, -1: none
     double due_at = -1.0;   // paced, >= 0: due this long after the job started
+    int seq = 0;            // position in the operator's transfer order (pooled jobs)
 };
 
 struct Job {
@@ -110,6 +114,9 @@ struct Job {
     bool wait_start = true;
     bool concurrent = false;         // paced: every item on a link of its own
     int final_flag = -1;             // flag published after every item landed
+    std::vector<int> more_finals;    // further such flags (a pooled job)
+    int pool_depth = 0;              // > 0: unpaced directions sharing every engine,
+                                     // at most this many copies queued per engine
 };
 
 struct Ctx;
@@ -128,6 +135,7 @@ struct Pacer {
     double lat_scale = 1.3;   // observed / modelled copy latency of paced items (biased late)
     void loop();
     void execute(Job &job);
+    void execute_pooled(Job &job);
     hsa_signal_t take_signal();
 };
 
@@ -148,6 +156,7 @@ struct Ctx {
     int grid_override = 0;
     int drop_flag = -1;
     int tile_override = 0;           // 0 auto, 1 256 x 256, 2 128 x 128
+    int pool_depth = kDefaultPoolDepth;   // unpaced directions share the engines (0: split)
     // optional HIP events around every GEMM launch (kernel durations)
     bool timing = false;
     static constexpr int kTimed = 512;
@@ -453,6 +462,10 @@ static size_t group_width(double rate, size_t E, size_t item_bytes) {
 void Pacer::execute(Job &job) {
     Ctx &c = *ctx;
     if (job.items.empty() && job.final_flag < 0) return;
+    if (job.pool_depth > 0) {
+        execute_pooled(job);
+        return;
+    }
     trace_event(role, job.epoch, "job_begin", -1, 0);
     if (job.wait_start && !spin_until_epoch(&c.hw[kHwStart], job.epoch, c.host_timeout)) {
         c.async_err.store(COMPASS_ERR_TIMEOUT);
@@ -600,6 +613,133 @@ void Pacer::execute(Job &job) {
             _mm_pause();
         }
     if (job.final_flag >= 0) __atomic_store_n(&c.hw[kHwFlags + job.final_flag], job.epoch, __ATOMIC_RELEASE);
+    trace_event(role, job.epoch, "landed", -1, 0);
+}
+
+// Pooled (unpaced directions sharing every engine): the job holds the items
+// of every active ring direction in the operator's transfer order. Each
+// engine keeps at most `pool_depth` copies queued; whenever one has room it
+// takes the next slice of the first item, in that order, that is ready (its
+// gate open) and has bytes left. An outgoing sum follows the incoming
+// partial of its partition in the order, so a finished chunk's send goes out
+// ahead of later arrivals, and no engine idles while either direction has
+// ready work (split per direction, the incoming fp32 partials and the gated
+// outgoing sums leave engines of one side idle while the other is behind).
+// Items are cut into equal slices of at most `slice` bytes; an item's flag is
+// published when all of its slices have landed.
+void Pacer::execute_pooled(Job &job) {
+    Ctx &c = *ctx;
+    trace_event(role, job.epoch, "job_begin", -1, 0);
+    if (job.wait_start && !spin_until_epoch(&c.hw[kHwStart], job.epoch, c.host_timeout)) {
+        c.async_err.store(COMPASS_ERR_TIMEOUT);
+        return;
+    }
+    trace_event(role, job.epoch, "start_seen", -1, 0);
+    const size_t E = job.engines.size();
+    const int depth = std::max(1, job.pool_depth);
+    struct State {
+        size_t off = 0, per = 0;
+        int inflight = 0;
+        bool ready = false, done = false;
+    };
+    struct Copy {
+        hsa_signal_t sg;
+        size_t item, eng;
+    };
+    std::vector<State> st(job.items.size());
+    size_t remaining = 0;
+    for (size_t i = 0; i < job.items.size(); ++i) {
+        const Item &it = job.items[i];
+        const size_t k = std::max<size_t>(1, (it.bytes + job.slice - 1) / job.slice);
+        st[i].per = std::max<size_t>(256, ((it.bytes + k - 1) / k + 255) & ~(size_t)255);
+        st[i].ready = it.gate < 0;
+        ++remaining;
+    }
+    std::vector<Copy> fly;
+    std::vector<int> load(E, 0);
+    size_t rr = 0, first_open = 0;
+    double last_progress = now_s();
+    while (remaining > 0) {
+        bool progress = false;
+        for (size_t i = 0; i < fly.size();) {
+            if (hsa_signal_load_scacquire(fly[i].sg) > 0) {
+                ++i;
+                continue;
+            }
+            --load[fly[i].eng];
+            State &s = st[fly[i].item];
+            --s.inflight;
+            fly[i] = fly.back();
+            fly.pop_back();
+            progress = true;
+        }
+        for (size_t i = first_open; i < job.items.size(); ++i) {
+            const Item &it = job.items[i];
+            State &s = st[i];
+            if (s.done) continue;
+            if (!s.ready && (int32_t)(__atomic_load_n(&c.hw[kHwDone + it.gate], __ATOMIC_ACQUIRE) - job.epoch) >= 0) {
+                s.ready = true;
+                progress = true;
+                trace_event(role, job.epoch, "gate_open", it.gate, 0);
+            }
+            if (s.ready && s.inflight == 0 && s.off >= it.bytes) {
+                if (it.flag >= 0) {
+                    __atomic_store_n(&c.hw[kHwFlags + it.flag], job.epoch, __ATOMIC_RELEASE);
+                    trace_event(role, job.epoch, "flag", it.flag, 0);
+                }
+                s.done = true;
+                --remaining;
+                progress = true;
+            }
+        }
+        while (first_open < job.items.size() && st[first_open].done) ++first_open;
+        for (;;) {
+            size_t e = E;
+            for (size_t k = 0; k < E; ++k) {
+                const size_t cand = (rr + k) % E;
+                if (load[cand] < depth && (e == E || load[cand] < load[e])) e = cand;
+            }
+            if (e == E) break;
+            size_t pick = job.items.size();
+            for (size_t i = first_open; i < job.items.size(); ++i)
+                if (st[i].ready && st[i].off < job.items[i].bytes) {
+                    pick = i;
+                    break;
+                }
+            if (pick == job.items.size()) break;
+            const Item &it = job.items[pick];
+            State &s = st[pick];
+            const size_t len = std::min(s.per, it.bytes - s.off);
+            hsa_signal_t sg = take_signal();
+            const hsa_status_t rc = hsa_amd_memory_async_copy_on_engine(
+                (char *)it.dst + s.off, it.dst_agent, (const char *)it.src + s.off, it.src_agent, len, 0, nullptr, sg,
+                (hsa_amd_sdma_engine_id_t)job.engines[e], true);
+            if (rc != HSA_STATUS_SUCCESS) {
+                hsa_signal_store_relaxed(sg, 0);
+                c.async_err.store(COMPASS_ERR_HIP);
+                return;
+            }
+            trace_event(role, job.epoch, "slice", __builtin_ctz(job.engines[e]), len);
+            fly.push_back({sg, pick, e});
+            ++load[e];
+            ++s.inflight;
+            s.off += len;
+            rr = e + 1;
+            progress = true;
+        }
+        if (progress) {
+            last_progress = now_s();
+        } else {
+            if (now_s() - last_progress > c.host_timeout) {
+                c.async_err.store(COMPASS_ERR_TIMEOUT);
+                return;
+            }
+            _mm_pause();
+        }
+    }
+    trace_event(role, job.epoch, "issued", -1, 0);
+    if (job.final_flag >= 0) __atomic_store_n(&c.hw[kHwFlags + job.final_flag], job.epoch, __ATOMIC_RELEASE);
+    for (int f : job.more_finals) __atomic_store_n(&c.hw[kHwFlags + f], job.epoch, __ATOMIC_RELEASE);
     trace_event(role, job.epoch, "landed", -1, 0);
 }
 
@@ -1104,6 +1244,7 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
             if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s
+            it.seq = j * geo.P + s;
             const bool on_fwd = a2a ? (c / dom == p->rank / dom) : part_fwd(geo, q);
             (on_fwd ? fwd : bwd)->items.push_back(it);
         }
@@ -1153,6 +1294,7 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      j * geo.P + q, -1);
             if (rc != COMPASS_OK) return rc;
             if (!due.empty()) it.due_at = due[(size_t)j * (p->n - 1) + (s - 1)];   // single ring: step s >= 1
+            it.seq = 2 * (j * geo.P + s) + 1;
             jobs[part_fwd(geo, q) ? 0 : 1].items.push_back(it);
         }
         if (!p->send_dst) continue;
@@ -1169,12 +1311,47 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
                                      (const char *)p->C + row * N * 2, (size_t)piece * N * 2, -1,
                                      gate_out ? j * geo.P + q : -1);
             if (rc != COMPASS_OK) return rc;
+            it.seq = 2 * (j * geo.P + s) + 2;   // right after its partition's incoming partial
             jobs[part_fwd(geo, q) ? 2 : 3].items.push_back(it);
         }
     }
     for (int r = 2; r < 4; ++r)
         if (!jobs[r].items.empty()) jobs[r].final_flag = kFinalFlag0 + r;
     return COMPASS_OK;
+}
+
+// Unpaced operators with more than one active direction let the directions
+// share every copy engine (COMPASS_OPT_POOL > 0): their items merge, in the
+// operator's transfer order, into the first such job, which runs pooled on
+// its role's thread; the other jobs are left empty. Paced links, per-hop due
+// times and the AlltoAll pattern keep a job per direction.
+static void pool_jobs(Job *jobs, int count) {
+    Ctx &c = g_ctx;
+    if (c.pool_depth <= 0) return;
+    int first = -1, active = 0;
+    for (int r = 0; r < count; ++r) {
+        if (jobs[r].items.empty()) continue;
+        if (jobs[r].rate > 0 || jobs[r].concurrent) return;
+        for (const Item &it : jobs[r].items)
+            if (it.due_at >= 0) return;
+        if (first < 0) first = r;
+        ++active;
+    }
+    if (active < 2) return;
+    Job &m = jobs[first];
+    for (int r = 0; r < count; ++r) {
+        if (r == first) continue;
+        for (Item &it : jobs[r].items) m.items.push_back(it);
+        jobs[r].items.clear();
+        if (jobs[r].final_flag >= 0) {
+            if (m.final_flag < 0) m.final_flag = jobs[r].final_flag;
+            else m.more_finals.push_back(jobs[r].final_flag);
+            jobs[r].final_flag = -1;
+        }
+    }
+    std::stable_sort(m.items.begin(), m.items.end(), [](const Item &a, const Item &b) { return a.seq < b.seq; });
+    m.engines = engines_for(first, std::vector<int>{first}, std::vector<int>{1}, 0);
+    m.pool_depth = c.pool_depth;
 }
 
 // Partitions in place before the operator starts: the rank's own chunk
@@ -1344,8 +1521,9 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = begin()) != COMPASS_OK) return rc;
     hipStream_t s = (hipStream_t)stream;
     const uint32_t epoch = next_epoch();
-    Job fwd, bwd;
-    if ((rc = ag_jobs(p, geo, l, epoch, 1, true, &fwd, &bwd)) != COMPASS_OK) return rc;
+    Job ag[2];
+    if ((rc = ag_jobs(p, geo, l, epoch, 1, true, &ag[0], &ag[1])) != COMPASS_OK) return rc;
+    pool_jobs(ag, 2);
     if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
@@ -1359,8 +1537,8 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
     g.start_word = &g_ctx.hw[kHwStart];
-    submit(0, std::move(fwd));
-    submit(1, std::move(bwd));
+    submit(0, std::move(ag[0]));
+    submit(1, std::move(ag[1]));
     return launch(g, cfg, false, s);
 }
 
@@ -1398,6 +1576,7 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
         for (int r = 2; r < 4; ++r)
             if (jobs[r].final_flag >= 0) finals.push_back(jobs[r].final_flag);
     }
+    pool_jobs(jobs, 4);
     for (int r = 0; r < 4; ++r) submit(r, std::move(jobs[r]));
     if ((rc = launch(g, cfg, true, s)) != COMPASS_OK) return rc;
     if (!finals.empty()) return join(epoch, finals, false, s);
@@ -1421,9 +1600,9 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
     const uint64_t res = resident_mask(p, geo);
     const int piece = geo.rows / d;   // rows of a chunk per sub-operator
     std::vector<int> finals;
-    Job ag_f, ag_b, rs[4];
+    Job agj[2], rs[4];
     if (p->pattern == COMPASS_AG_GEMM) {
-        if ((rc = ag_jobs(p, geo, l, epoch, d, true, &ag_f, &ag_b)) != COMPASS_OK) return rc;
+        if ((rc = ag_jobs(p, geo, l, epoch, d, true, &agj[0], &agj[1])) != COMPASS_OK) return rc;
         if ((rc = stage_local_shard(p, geo, s)) != COMPASS_OK) return rc;
     } else {
         if ((rc = rs_jobs(p, geo, l, epoch, d, res, true, true, rs)) != COMPASS_OK) return rc;
@@ -1461,9 +1640,11 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
         set_split(g, cfg);
     }
     if (p->pattern == COMPASS_AG_GEMM) {
-        submit(0, std::move(ag_f));
-        submit(1, std::move(ag_b));
+        pool_jobs(agj, 2);
+        submit(0, std::move(agj[0]));
+        submit(1, std::move(agj[1]));
     } else {
+        pool_jobs(rs, 4);
         for (int r = 0; r < 4; ++r) submit(r, std::move(rs[r]));
     }
     for (int j = 0; j < d; ++j)
@@ -1498,13 +1679,14 @@ int op_transfer(const compass_problem *p, const compass_links *l, void *stream) 
     const uint32_t epoch = next_epoch();
     std::vector<int> wait;
     if (p->pattern == COMPASS_AG_GEMM) {
-        Job f, b;
-        if ((rc = ag_jobs(p, geo, l, epoch, 1, true, &f, &b)) != COMPASS_OK) return rc;
-        for (auto &it : f.items) wait.push_back(it.flag);
-        for (auto &it : b.items) wait.push_back(it.flag);
+        Job ag[2];
+        if ((rc = ag_jobs(p, geo, l, epoch, 1, true, &ag[0], &ag[1])) != COMPASS_OK) return rc;
+        for (int r = 0; r < 2; ++r)
+            for (auto &it : ag[r].items) wait.push_back(it.flag);
         if ((rc = join(epoch, wait, true, s)) != COMPASS_OK) return rc;
-        submit(0, std::move(f));
-        submit(1, std::move(b));
+        pool_jobs(ag, 2);
+        submit(0, std::move(ag[0]));
+        submit(1, std::move(ag[1]));
     } else {
         Job jobs[4];
         if ((rc = rs_jobs(p, geo, l, epoch, 1, resident_mask(p, geo), false, true, jobs)) != COMPASS_OK) return rc;
@@ -1513,6 +1695,7 @@ int op_transfer(const compass_problem *p, const compass_links *l, void *stream) 
         for (int r = 2; r < 4; ++r)
             if (jobs[r].final_flag >= 0) wait.push_back(jobs[r].final_flag);
         if ((rc = join(epoch, wait, true, s)) != COMPASS_OK) return rc;
+        pool_jobs(jobs, 4);
         for (int r = 0; r < 4; ++r) submit(r, std::move(jobs[r]));
     }
     return COMPASS_OK;
@@ -1543,6 +1726,7 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
     for (int r = 2; r < 4; ++r)
         if (jobs[r].final_flag >= 0) wait.push_back(jobs[r].final_flag);
     if ((rc = join(epoch, wait, true, s)) != COMPASS_OK) return rc;
+    pool_jobs(jobs, 4);
     for (int r = 0; r < 4; ++r) submit(r, std::move(jobs[r]));
     return COMPASS_OK;
 }
@@ -1581,6 +1765,10 @@ int op_set_option(int key, long long v) {
     case COMPASS_OPT_TILE:
         if (v < 0 || v > 2) return set_error(COMPASS_ERR_INVALID, "tile option must be 0, 1 or 2");
         c.tile_override = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_POOL:
+        if (v < 0 || v > 8) return set_error(COMPASS_ERR_INVALID, "pool option must lie in [0, 8]");
+        c.pool_depth = (int)v;
         return COMPASS_OK;
     case COMPASS_OPT_ENGINE_MASK:
         if (v < 0 || v > 0xFFFF) return set_error(COMPASS_ERR_INVALID, "engine mask out of range");

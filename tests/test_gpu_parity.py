@@ -789,3 +789,73 @@ def test_sub_chunks_sequential_transfer_and_decomp_d1():
     C.compass_sequential(case.problem, lk)
     C.compass_sync()
     assert np.array_equal(host_bits(case.C), rref)
+
+
+# ------------------------------------------------------------ unpaced directions sharing the copy engines
+@pytest.fixture
+def pool_depth(request):
+    C.compass_set_option(C.OPT_POOL, request.param)
+    yield request.param
+    C.compass_set_option(C.OPT_POOL, 2)
+
+
+UNPACED = C.links(0.0, 0.0, slice_bytes=64 << 10)   # small slices: several per item
+
+
+@pytest.mark.parametrize("pool_depth", [0, 1, 2], indirect=True)
+@pytest.mark.parametrize("ring", ["double", "double_split"])
+def test_pooled_ag_gemm_integer_exact_all_ranks(pool_depth, ring):
+    for bad in (-1, 9):
+        with pytest.raises(C.CompassError):
+            C.compass_set_option(C.OPT_POOL, bad)
+    n = 8
+    inp = make_int_ag_inputs(2048, 264, 328, n, seed=181)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    for rank in range(n):
+        _say("pooled ag", pool_depth, ring, rank)
+        case = AGCase(inp, rank, ring, pinned_remote=rank % 2 == 1)
+        C.compass_ag_gemm(case.problem, UNPACED)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), rank
+    for d in (2, 4):
+        case = AGCase(inp, 3, ring)
+        C.compass_decomp_gemm(case.problem, d, UNPACED)
+        C.compass_sync()
+        assert np.array_equal(host_bits(case.C), ref), d
+
+
+@pytest.mark.parametrize("pool_depth", [0, 1, 2], indirect=True)
+@pytest.mark.parametrize("ring", ["single", "double"])
+def test_pooled_gemm_rs_with_sends_integer_exact(pool_depth, ring):
+    # the incoming partials and the gated outgoing sums in one pooled job:
+    # every chunk sum and every sent chunk bit-exact, on every rank, fused and
+    # through InterDecom; then the unfused operator and the transfer alone
+    n = 8
+    rin = make_int_rs_inputs(2048, 264, 136, n, seed=182)
+    rref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(rin["A"]), O.bf16_to_f64(rin["W"]),
+                                       [p.astype(np.float64) for p in rin["P_in"]], n))
+    rows = 2048 // n
+
+    def check(case, tag):
+        assert np.array_equal(host_bits(case.C), rref), tag
+        for q in range(n):
+            if q != case.rank:
+                assert np.array_equal(host_bits(case.send[q]), rref[q * rows:(q + 1) * rows]), (tag, q)
+
+    for rank in range(n):
+        _say("pooled rs", pool_depth, ring, rank)
+        case = RSCase(rin, rank, ring)
+        C.compass_gemm_rs(case.problem, UNPACED)
+        C.compass_sync()
+        check(case, ("fused", rank))
+    for d in (2, 4):
+        case = RSCase(rin, 5, ring)
+        C.compass_decomp_gemm(case.problem, d, UNPACED)
+        C.compass_sync()
+        check(case, ("decomp", d))
+    case = RSCase(rin, 6, ring)
+    C.compass_transfer(case.problem, UNPACED)   # stages the partials for the unfused epilogue
+    C.compass_sync()
+    C.compass_sequential(case.problem, UNPACED)
+    C.compass_sync()
+    check(case, "sequential")
