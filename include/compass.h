@@ -125,11 +125,13 @@ int compass_schedule(int pattern, int ring, int n, int rank, int32_t *out, int c
  * measure).
  * Unpaced (rate <= 0): copies go out as fast as the engines take them, in
  * slices round-robin over the engines; flags publish when the data landed.
- * Rates in (0, 1e8) are rejected.
+ * With more than one active direction the directions share every engine
+ * (COMPASS_OPT_POOL). Rates in (0, 1e8) are rejected.
  *
- * slice_bytes: largest single copy (0: library default, 2 MiB; else
- * >= 4 KiB). engines_per_ring: SDMA engines per ring direction (0: library
- * default, all usable engines split over the active directions).
+ * slice_bytes: largest single copy (0: library default, 2 MiB, or 3 MiB for
+ * unpaced directions sharing the engines; else >= 4 KiB). engines_per_ring:
+ * SDMA engines per ring direction (0: library default, all usable engines
+ * split over the active directions; not used when they share the engines).
  *
  * hop_Bps (single ring only; NULL: every hop at fwd_Bps): n rates, hop q
  * carrying rank q -> q+1 mod n, each >= 1e8 (paced), for a ring whose hops
@@ -298,9 +300,10 @@ int compass_sync(void);
                                        engine with at most this many copies queued, slices
                                        taken in transfer order (an outgoing sum right after
                                        its partition's incoming partial) from items that are
-                                       ready; 0 = the engines split per direction in
-                                       proportion to their bytes (default 2: a queued copy
-                                       hides the copy side's reaction time; at most 8) */
+                                       ready, in slices of 3 MiB unless the links set
+                                       slice_bytes; 0 = the engines split per direction in
+                                       proportion to their bytes (default 4: queued copies
+                                       hide the copy side's reaction time; at most 8) */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

@@ -4,7 +4,7 @@
     python -m paper_2609_10549_amd.profile_summary traffic <fetch_dir> <write_dir> <copy_fetch_dir> \
         <copy_write_dir> <kernel substring> <out.json> [command that made each dir ...]
     python -m paper_2609_10549_amd.profile_summary mfma <counter_dir> <copy_trace_dir> <last_n> <out.md> \
-        <command...>
+        <job_bytes> <command...>
 
 `trace` averages the last `last_n` dispatches of every kernel (the timed
 steps of `bench.py --profile-only`). `traffic` converts the FETCH_SIZE and
@@ -14,8 +14,11 @@ and records a hash of the kernel source the counters were taken with. `mfma`
 reports MfmaUtil (matrix-core busy cycles over active cycles of every SIMD)
 and the bf16 MFMA work of every GEMM kernel, averaged over its last `last_n`
 dispatches, and the SDMA side from a memory-copy trace: device-to-device
-copies grouped into transfer jobs (gaps above 30 us split them), each copy
-2 MiB (the unpaced slice size every benchmark copy uses)."""
+copies grouped into transfer jobs (gaps above 30 us split them). The trace
+holds no sizes: `job_bytes` lists the jobs of one benchmark step as
+bytes:copies pairs, comma-separated; a traced job with one of those copy
+counts is taken to move those bytes in equal parts, and a job with another
+count (a gap that split one) is listed without them."""
 from __future__ import annotations
 
 import csv
@@ -81,10 +84,10 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, kernel_sub, out, *comm
     print(json.dumps(rec))
 
 
-SLICE_BYTES = 2 << 20
 
 
-def mfma(counter_dir, copy_dir, last_n, out, command):
+def mfma(counter_dir, copy_dir, last_n, out, job_bytes, command):
+    kinds = {int(c): int(b) for b, c in (x.split(":") for x in job_bytes.split(","))}
     by = defaultdict(lambda: defaultdict(list))
     for path in glob.glob(os.path.join(counter_dir, "*counter_collection.csv")):
         for r in csv.DictReader(open(path)):
@@ -117,19 +120,30 @@ def mfma(counter_dir, copy_dir, last_n, out, command):
     if cur:
         jobs.append(cur)
     tail = jobs[-last_n:]
-    dur = sorted((e - b) / 1e3 for j in tail for b, e in j)
-    pct = lambda q: dur[min(len(dur) - 1, int(q * len(dur)))]  # noqa: E731
+    per_kind = defaultdict(list)
+    for j in tail:
+        if len(j) in kinds:
+            per_kind[len(j)].extend((e - b) / 1e3 for b, e in j)
     lines += ["", f"SDMA device-to-device copies: {len(copies)} in {len(jobs)} transfer jobs; the last {len(tail)} "
-              "jobs:", "",
-              f"* per copy (2 MiB): duration p10 / p50 / p90 = {pct(0.1):.1f} / {pct(0.5):.1f} / {pct(0.9):.1f} us, "
-              f"i.e. {SLICE_BYTES / pct(0.5) / 1e3:.1f} GB/s per copy at the median",
-              "", "The memory-copy tracer intercepts every copy call on the host, which stretches a job's "
+              "jobs:", ""]
+    for ncopy, v in kinds.items():
+        dur = sorted(per_kind.get(ncopy, []))
+        if not dur:
+            continue
+        size = v / ncopy
+        pct = lambda q: dur[min(len(dur) - 1, int(q * len(dur)))]  # noqa: E731
+        lines.append(f"* jobs of {v / 2**20:.0f} MiB in {ncopy} copies of {size / 2**20:.2f} MiB: duration "
+                     f"p10 / p50 / p90 = {pct(0.1):.1f} / {pct(0.5):.1f} / {pct(0.9):.1f} us, "
+                     f"i.e. {size / pct(0.5) / 1e3:.1f} GB/s per copy at the median")
+    lines += ["", "The memory-copy tracer intercepts every copy call on the host, which stretches a job's "
               "span against an untraced run (the benchmark's own transfer-alone times are the reference); the "
               "per-copy durations are the engines' own.", "",
-              "| job | copies | span us | aggregate GB/s |", "|---|---|---|---|"]
+              "| job | MiB | copies | span us | aggregate GB/s |", "|---|---|---|---|---|"]
     for i, j in enumerate(tail):
         span = (max(e for _, e in j) - min(b for b, _ in j)) / 1e3
-        lines.append(f"| {i} | {len(j)} | {span:.1f} | {len(j) * SLICE_BYTES / span / 1e3:.1f} |")
+        v = kinds.get(len(j))
+        mib, rate = (f"{v / 2**20:.0f}", f"{v / span / 1e3:.1f}") if v else ("?", "?")
+        lines.append(f"| {i} | {mib} | {len(j)} | {span:.1f} | {rate} |")
     lines += ["", f"Kernel source hash: {kernel_source_hash()}"]
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
@@ -139,6 +153,6 @@ if __name__ == "__main__":
     if sys.argv[1] == "trace":
         trace(sys.argv[2], int(sys.argv[3]), sys.argv[4], " ".join(sys.argv[5:]))
     elif sys.argv[1] == "mfma":
-        mfma(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], " ".join(sys.argv[6:]))
+        mfma(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))
     else:
         traffic(*sys.argv[2:])

@@ -796,13 +796,13 @@ def test_sub_chunks_sequential_transfer_and_decomp_d1():
 def pool_depth(request):
     C.compass_set_option(C.OPT_POOL, request.param)
     yield request.param
-    C.compass_set_option(C.OPT_POOL, 2)
+    C.compass_set_option(C.OPT_POOL, 4)
 
 
 UNPACED = C.links(0.0, 0.0, slice_bytes=64 << 10)   # small slices: several per item
 
 
-@pytest.mark.parametrize("pool_depth", [0, 1, 2], indirect=True)
+@pytest.mark.parametrize("pool_depth", [0, 1, 4], indirect=True)
 @pytest.mark.parametrize("ring", ["double", "double_split"])
 def test_pooled_ag_gemm_integer_exact_all_ranks(pool_depth, ring):
     for bad in (-1, 9):
@@ -824,7 +824,7 @@ def test_pooled_ag_gemm_integer_exact_all_ranks(pool_depth, ring):
         assert np.array_equal(host_bits(case.C), ref), d
 
 
-@pytest.mark.parametrize("pool_depth", [0, 1, 2], indirect=True)
+@pytest.mark.parametrize("pool_depth", [0, 1, 4], indirect=True)
 @pytest.mark.parametrize("ring", ["single", "double"])
 def test_pooled_gemm_rs_with_sends_integer_exact(pool_depth, ring):
     # the incoming partials and the gated outgoing sums in one pooled job:
