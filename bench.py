@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--strategy", choices=["auto", "fusion", "decomp", "sequential"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--remote", choices=["device", "host"], default="device",
+                    help="where the other ranks' shards, partials and send buffers live: separate HBM "
+                         "allocations (default) or pinned host memory (every transfer crosses PCIe)")
     ap.add_argument("--profile-only", action="store_true",
                     help="run only the timed steps (for rocprofv3); print the JSON line")
     return ap.parse_args()
@@ -72,12 +75,18 @@ def main():
     def bits(x):
         return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(dev)
 
+    host_remote = args.remote == "host"
+
+    def remote(t):
+        """Another rank's buffer: a separate device allocation, or pinned host memory."""
+        return t.cpu().pin_memory() if host_remote else t
+
     n = ag_in["n"]
     M1, N1, K1 = ag_in["M"], ag_in["N"], ag_in["K"]
     rows1 = M1 // n
     gathered = torch.empty((M1, K1), dtype=torch.int16, device=dev)
     gathered[rank * rows1:(rank + 1) * rows1] = bits(ag_in["shards"][rank])
-    shards = [gathered[rank * rows1:(rank + 1) * rows1] if q == rank else bits(ag_in["shards"][q])
+    shards = [gathered[rank * rows1:(rank + 1) * rows1] if q == rank else remote(bits(ag_in["shards"][q]))
               for q in range(n)]
     W1 = bits(ag_in["W"])
     C1 = torch.empty((M1, N1), dtype=torch.int16, device=dev)
@@ -89,12 +98,13 @@ def main():
     W2 = bits(rs_in["W"])
     C2 = torch.empty((M2, N2), dtype=torch.int16, device=dev)
     stage = torch.empty((M2, N2), dtype=torch.float32, device=dev)
-    partials = [torch.from_numpy(p).to(dev) for p in rs_in["P_in"]]
+    partials = [remote(torch.from_numpy(p).to(dev)) for p in rs_in["P_in"]]
     # the first ReduceScatter step's partial is resident: point it at its stage rows
     first = C.compass_schedule("rs", "single", n, rank)[0]
     stage[first * rows2:(first + 1) * rows2] = partials[first]
     partials[first] = stage[first * rows2:(first + 1) * rows2]
-    sends = [None if q == rank else torch.empty((rows2, N2), dtype=torch.int16, device=dev) for q in range(n)]
+    sends = [None if q == rank else remote(torch.empty((rows2, N2), dtype=torch.int16, device=dev))
+             for q in range(n)]
     p_rs = C.rs_problem(A2, W2, partials, stage, C2, sends, rank, "single")
     torch.cuda.synchronize()
 
@@ -213,7 +223,8 @@ def main():
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "tp8_mlp_fwd_rank_share: fc1 AG-GEMM 8192x2048x4096 double ring + "
                                "fc2 GEMM-RS 8192x4096x2048 single ring",
-                   "global_batch": 4, "seq_len": 2048, "parallelism": "tp8 (one rank emulated)"},
+                   "global_batch": 4, "seq_len": 2048, "parallelism": "tp8 (one rank emulated)",
+                   "remote": "pinned host (PCIe)" if host_remote else "device (HBM)"},
         "roofline": roofline,
     }
     if args.profile_only:

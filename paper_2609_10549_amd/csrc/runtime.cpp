@@ -1331,7 +1331,12 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
 // share every copy engine (COMPASS_OPT_POOL > 0): their items merge, in the
 // operator's transfer order, into the first such job, which runs pooled on
 // its role's thread; the other jobs are left empty. Paced links, per-hop due
-// times and the AlltoAll pattern keep a job per direction.
+// times and the AlltoAll pattern keep a job per direction, and so do copies
+// to or from host memory: across PCIe the link, not the engines, is the
+// limit, a copy takes milliseconds, and a pooled engine's queue would hold
+// an outgoing sum behind incoming partials that a direction of its own
+// sends past (the fc2 ReduceScatter with pinned-host remote buffers: fused
+// 3.03 ms pooled against the unfused 2.53 ms).
 static void pool_jobs(Job *jobs, int count) {
     Ctx &c = g_ctx;
     if (c.pool_depth <= 0) return;
@@ -1340,7 +1345,7 @@ static void pool_jobs(Job *jobs, int count) {
         if (jobs[r].items.empty()) continue;
         if (jobs[r].rate > 0 || jobs[r].concurrent) return;
         for (const Item &it : jobs[r].items)
-            if (it.due_at >= 0) return;
+            if (it.due_at >= 0 || it.src_agent.handle != c.gpu.handle || it.dst_agent.handle != c.gpu.handle) return;
         if (first < 0) first = r;
         ++active;
     }
