@@ -1,0 +1,108 @@
+"""Host-side checks of the benchmark's contract and of the rocprofv3 summary
+tool (no GPU): the one-GPU refusal, the traffic record's kernel-source gate,
+and the summaries computed from small hand-made rocprofv3 CSV files."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
+    assert r.stdout == ""
+
+
+def test_stored_traffic_follows_the_kernel_source(monkeypatch):
+    import bench
+    from paper_2609_10549_amd import profile_summary as PS
+    with open(os.path.join(ROOT, "profiles", "traffic_rs.json")) as f:
+        rec = json.load(f)
+    monkeypatch.setattr(PS, "kernel_source_hash", lambda: rec["kernel_source_hash"])
+    assert bench.stored_traffic("rs") == round(rec["traffic_bytes_per_launch"], 0)
+    monkeypatch.setattr(PS, "kernel_source_hash", lambda: "0" * 16)
+    assert bench.stored_traffic("rs") is None
+    assert bench.stored_traffic("no_such_kernel") is None
+
+
+def _write(path, header, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+def test_trace_summary_averages_the_last_dispatches(tmp_path):
+    from paper_2609_10549_amd import profile_summary as PS
+    rows = [["void compass::gemm_kernel<128, 128, true>(compass::GemmParams)", 1000 * i, 1000 * i + d]
+            for i, d in enumerate([9000, 100_000, 200_000, 300_000])]
+    rows.append(["join_kernel", 0, 4000])
+    src = tmp_path / "kt.csv"
+    _write(src, ["Kernel_Name", "Start_Timestamp", "End_Timestamp"], rows)
+    out = tmp_path / "t.md"
+    PS.trace(str(src), 3, str(out), "cmd line")
+    text = out.read_text()
+    assert "Command: `cmd line`" in text
+    # the last three dispatches: 100, 200, 300 us
+    assert "| `compass::gemm_kernel<128, 128, true>` | 3 | 200.0 | 100.0 | 300.0 |" in text
+    assert "| `join_kernel` | 1 | 4.0 | 4.0 | 4.0 |" in text
+    assert f"Kernel source hash: {PS.kernel_source_hash()}" in text
+
+
+def test_copy_summary_classifies_jobs_by_copy_count(tmp_path):
+    from paper_2609_10549_amd import profile_summary as PS
+    cdir = tmp_path / "counters"
+    cdir.mkdir()
+    _write(cdir / "b_counter_collection.csv", ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"],
+           [[1, "void compass::gemm_kernel<128, 128, true>(x)", "MfmaUtil", 20.0],
+            [1, "void compass::gemm_kernel<128, 128, true>(x)", "SQ_INSTS_VALU_MFMA_MOPS_BF16", 2.0e9 / 512]])
+    tdir = tmp_path / "copies"
+    tdir.mkdir()
+    rows = []
+    t = 0
+    # a job of 2 copies of 1 MiB each 10 us, a job of 4 copies each 20 us, a job of 3 (unknown)
+    for n, dur in ((2, 10_000), (4, 20_000), (3, 5_000)):
+        for _ in range(n):
+            rows.append(["MEMORY_COPY", "MEMORY_COPY_DEVICE_TO_DEVICE", t, t + dur])
+            t += 1_000
+        t += 100_000   # a gap that separates the jobs
+    _write(tdir / "b_memory_copy_trace.csv", ["Kind", "Direction", "Start_Timestamp", "End_Timestamp"], rows)
+    out = tmp_path / "m.md"
+    PS.mfma(str(cdir), str(tdir), 20, str(out), f"{2 << 20}:2,{8 << 20}:4", "cmd")
+    text = out.read_text()
+    assert "| `compass::gemm_kernel<128, 128, true>` | 1 | 20.0 | 2.0 |" in text
+    assert "jobs of 2 MiB in 2 copies of 1.00 MiB: duration p10 / p50 / p90 = 10.0 / 10.0 / 10.0 us" in text
+    assert "jobs of 8 MiB in 4 copies of 2.00 MiB" in text
+    table = [ln for ln in text.splitlines() if ln.startswith("| 0 ") or ln.startswith("| 1 ") or ln.startswith("| 2 ")]
+    assert table[0].startswith("| 0 | 2 | 2 | 11.0 |")    # span 0 .. 11 us
+    assert table[1].startswith("| 1 | 8 | 4 | 23.0 |")
+    assert table[2] == "| 2 | ? | 3 | 7.0 | ? |"
+
+
+def test_traffic_summary_scales_by_the_copy_probe(tmp_path):
+    from paper_2609_10549_amd import profile_summary as PS
+    dirs = {}
+    for name, kernel, value in (("f", "gemm_kernel<128, 128, true>", 1000.0), ("w", "gemm_kernel<128, 128, true>", 300.0),
+                                ("cf", "copy_kernel", PS.COPY_BYTES / 2 / 1024), ("cw", "copy_kernel", PS.COPY_BYTES / 1024)):
+        d = tmp_path / name
+        d.mkdir()
+        counter = "FETCH_SIZE" if name in ("f", "cf") else "WRITE_SIZE"
+        _write(d / "x_counter_collection.csv", ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"],
+               [[1, kernel, counter, value], [2, kernel, counter, value]])
+        dirs[name] = str(d)
+    out = tmp_path / "t.json"
+    PS.traffic(dirs["f"], dirs["w"], dirs["cf"], dirs["cw"], "gemm_kernel<128, 128, true>", str(out), "c1")
+    rec = json.loads(out.read_text())
+    assert rec["fetch_scale"] == pytest.approx(2.0)
+    assert rec["write_scale"] == pytest.approx(1.0)
+    assert rec["fetch_bytes_per_launch"] == pytest.approx(1000.0 * 1024 * 2)
+    assert rec["write_bytes_per_launch"] == pytest.approx(300.0 * 1024)
+    assert rec["commands"] == ["c1"]
+    assert rec["kernel_source_hash"] == PS.kernel_source_hash()
