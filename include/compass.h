@@ -304,6 +304,10 @@ int compass_sync(void);
                                        slice_bytes; 0 = the engines split per direction in
                                        proportion to their bytes (default 4: queued copies
                                        hide the copy side's reaction time; at most 8) */
+#define COMPASS_OPT_PACE_HEADROOM 12 /* paced links: the engines of a direction form groups
+                                       of k per item, the widest k whose groups carry the
+                                       link rate with this many per cent to spare (0..100,
+                                       default 5); wider groups land each item sooner */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

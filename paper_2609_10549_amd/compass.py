@@ -37,6 +37,7 @@ OPT_KERNEL_TIMING = 7
 OPT_TILE_TRACE = 8
 OPT_SCHED = 9
 OPT_POOL = 10
+OPT_PACE_HEADROOM = 12
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RING_DOUBLE_SPLIT = 2
