@@ -432,8 +432,10 @@ constexpr double kEngineBps = 38e9;
 
 // Engines per item for a paced job: the widest group (shortest item latency)
 // whose E / k groups still carry the link rate with `headroom` to spare; if
-// none does, all E engines per item (the rate is then out of reach anyway,
-// and narrower groups would only add latency). The first items of a job are
+// none does, one engine per item: the rate is then out of reach, and single
+// copies, E at a time, pay the fixed cost of a copy least often, so the link
+// comes closest to it (all E engines per small item would carry a fraction
+// of what single copies do). The first items of a job are
 // issued at once and land one group latency after the start, so too narrow
 // a group delays them all: at 268 GB/s with 22 MiB items, 10 % headroom left
 // groups of 2 engines (≈ 310 µs per item) where 5 % allows 4 (≈ 160 µs), and
@@ -444,7 +446,7 @@ static size_t group_width(double rate, size_t E, size_t item_bytes, double headr
         const double lat = kCopyFixed + (double)item_bytes / ((double)k * kEngineBps);
         if ((double)(E / k) * (double)item_bytes / lat >= (1.0 + headroom) * rate) return k;
     }
-    return E;
+    return 1;
 }
 
 // One job.
