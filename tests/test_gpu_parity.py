@@ -412,6 +412,48 @@ def test_probe_mfma_reports_a_plausible_rate_and_clock():
 
 
 # ------------------------------------------------------------ paced links and the tile trace
+def test_pacing_headroom_and_an_unreachable_rate():
+    # the headroom option's range; a rate no group of engines can carry (tiny
+    # items at 1 TB/s per ring) runs one engine per item and lands every
+    # partition, not far behind the unpaced transfer; any headroom delivers
+    for bad in (-1, 101):
+        with pytest.raises(C.CompassError):
+            C.compass_set_option(C.OPT_PACE_HEADROOM, bad)
+    n = 8
+    M, N, K = 4096, 64, 1024
+    inp = make_ag_inputs(M, N, K, n, seed=65)
+    case = AGCase(inp, 5, "double")
+    fast, unpaced = C.links(1e12, 1e12), C.links(0.0, 0.0)
+
+    def best(lk):
+        C.compass_transfer(case.problem, lk)   # warm
+        C.compass_sync()
+        t = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            C.compass_transfer(case.problem, lk)
+            b.record()
+            b.synchronize()
+            C.compass_sync()
+            t.append(a.elapsed_time(b) * 1e-3)
+        return min(t)
+
+    try:
+        for h in (0, 5, 100):
+            C.compass_set_option(C.OPT_PACE_HEADROOM, h)
+            rows = M // n   # clear the remote rows (the local shard stays in place)
+            case.gathered.zero_()
+            case.gathered[5 * rows:6 * rows] = dev_bits(inp["shards"][5])
+            t_fast = best(fast)
+            assert np.array_equal(host_bits(case.gathered), np.vstack(inp["shards"])), h
+        t_unpaced = best(unpaced)
+        _say("unreachable rate", t_fast, "unpaced", t_unpaced)
+        assert t_fast < 2.0 * t_unpaced + 1e-3
+    finally:
+        C.compass_set_option(C.OPT_PACE_HEADROOM, 5)
+
+
 def test_paced_link_never_beats_its_rate():
     # 7 items of 512 KiB per ring direction at 20 GB/s: the last flag is due
     # after 7 * 512 KiB / rate, and a paced link publishes none earlier
