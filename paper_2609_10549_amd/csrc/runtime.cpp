@@ -143,6 +143,7 @@ struct Pacer {
     void execute(Job &job);
     void execute_pooled(Job &job);
     hsa_signal_t take_signal();
+    void quiesce();
 };
 
 struct Ctx {
@@ -388,6 +389,18 @@ hsa_signal_t Pacer::take_signal() {
     return s;
 }
 
+// Wait until every copy issued with this pacer's signals has completed
+// (bounded: the host timeout, at least one second, since the timeout may be
+// what ended the job).
+void Pacer::quiesce() {
+    const double t0 = now_s(), bound = std::max(1.0, ctx->host_timeout);
+    for (int i = 0; i < kSignals; ++i)
+        while (hsa_signal_load_scacquire(sig[i]) > 0) {
+            if (now_s() - t0 > bound) return;
+            _mm_pause();
+        }
+}
+
 void Pacer::loop() {
     double idle_since = now_s();
     while (!stop.load()) {
@@ -408,6 +421,10 @@ void Pacer::loop() {
             q.pop_front();
         }
         execute(job);
+        // a job that ended on an error may have left copies in flight: let them
+        // land before the job counts as done, so that compass_sync() returns
+        // with none of them still writing the caller's buffers
+        if (ctx->async_err.load() != 0) quiesce();
         pending.fetch_sub(1, std::memory_order_acq_rel);
         idle_since = now_s();
     }
@@ -785,8 +802,6 @@ static int take_async_error() {
 
 static uint32_t next_epoch() { return ++g_ctx.epoch; }
 
-// SDMA engines of one ring direction: the usable engines are split evenly
-// over the directions active in the operator (`active` lists their roles).
 // SDMA engines of one ring direction: the usable engines are split over the
 // directions active in the operator in proportion to the bytes each carries
 // (`active` lists their roles, `weight` their relative traffic).

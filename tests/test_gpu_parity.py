@@ -901,3 +901,37 @@ def test_pooled_gemm_rs_with_sends_integer_exact(pool_depth, ring):
     C.compass_sequential(case.problem, UNPACED)
     C.compass_sync()
     check(case, "sequential")
+
+
+@pytest.mark.parametrize("pool_depth", [0, 4], indirect=True)
+def test_copy_side_timeout_then_recovers(pool_depth):
+    # a copy-side wait bound of 1 us: the ReduceScatter's copy side gives up
+    # between its first copies and their landing (or at a chunk-done gate),
+    # lets the copies it issued land, and the kernel then times out on the
+    # partials whose flags never come. compass_sync reports the timeout; the
+    # next call, with the bounds restored, is bit-exact, sends included
+    n = 4
+    rin = make_int_rs_inputs(1024, 264, 136, n, seed=190)
+    rref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(rin["A"]), O.bf16_to_f64(rin["W"]),
+                                       [p.astype(np.float64) for p in rin["P_in"]], n))
+    rows = 1024 // n
+    C.compass_set_option(C.OPT_SPIN_LIMIT, 20000)
+    C.compass_set_option(C.OPT_HOST_TIMEOUT, 1)
+    try:
+        _say("copy-side timeout case", pool_depth)
+        case = RSCase(rin, 1, "double")
+        C.compass_gemm_rs(case.problem, UNPACED)
+        with pytest.raises(C.CompassError) as e:
+            C.compass_sync()
+        assert e.value.code == C.ERR_TIMEOUT
+    finally:
+        C.compass_set_option(C.OPT_HOST_TIMEOUT, 5_000_000)
+        C.compass_set_option(C.OPT_SPIN_LIMIT, 4 << 20)
+    _say("copy-side recovery case", pool_depth)
+    case = RSCase(rin, 1, "double")
+    C.compass_gemm_rs(case.problem, UNPACED)
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), rref)
+    for q in range(n):
+        if q != 1:
+            assert np.array_equal(host_bits(case.send[q]), rref[q * rows:(q + 1) * rows]), q
