@@ -31,6 +31,16 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(C._SIGS), "binding and header disagree"
 
 
+def test_every_header_constant_has_the_same_value_in_the_binding():
+    text = open(os.path.join(ROOT, "include", "compass.h")).read()
+    defs = dict(re.findall(r"^#define COMPASS_([A-Z0-9_]+)\s+(-?\d+)\b", text, flags=re.M))
+    assert len(defs) >= 24
+    for name, value in defs.items():
+        assert getattr(C, name) == int(value), name
+    opts = {k: v for k, v in defs.items() if k.startswith("OPT_")}
+    assert len(set(opts.values())) == len(opts), "two options share a key"
+
+
 def test_struct_sizes_match_c_layout():
     assert ctypes.sizeof(C.compass_links) == 40
     assert ctypes.sizeof(C.compass_problem) == 4 * 7 + 4 + 8 * 8
