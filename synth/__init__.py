@@ -13,4 +13,5 @@ from .gen import (  # noqa: F401
     make_int_ag_inputs,
     make_int_rs_inputs,
     make_config_inputs,
+    make_int_config_inputs,
 )

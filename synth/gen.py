@@ -21,7 +21,7 @@ import numpy as np
 
 __all__ = [
     "CONFIGS", "bf16_bits", "config_shapes", "make_ag_inputs", "make_rs_inputs",
-    "make_int_ag_inputs", "make_int_rs_inputs", "make_config_inputs",
+    "make_int_ag_inputs", "make_int_rs_inputs", "make_config_inputs", "make_int_config_inputs",
 ]
 
 
@@ -136,3 +136,21 @@ def make_config_inputs(idx: int, pattern: str | None = None) -> dict:
         return make_ag_inputs(c["M"], c["N"], c["K"], c["n"], c["seed"], c["dist_a"], c["dist_w"])
     return make_rs_inputs(c["M"], c["N"], c["K"], c["n"], c["seed"], c["dist_a"],
                           c["dist_w"], c["dist_p"])
+
+
+def make_int_config_inputs(idx: int, pattern: str | None = None) -> dict:
+    """Configuration ``idx`` at its full shape with small-integer values
+    (activations and weights in [-4, 4], partials in [-64, 64]): every fp32
+    partial sum of the product is exact (|sum| <= 16 K + 64 < 2**24 for
+    K <= 12288), so a correct GEMM's bf16 output is the exact result rounded
+    once. Seeds differ from the seeded-normal inputs of the same shape."""
+    c = CONFIGS[idx]
+    if idx == 5:
+        sh = c[pattern]
+        M, N, K, pat = sh["M"], sh["N"], sh["K"], pattern
+    else:
+        M, N, K, pat = c["M"], c["N"], c["K"], c["pattern"]
+    seed = 1000 + 10 * idx + (1 if pat == "rs" else 0)
+    if pat == "ag":
+        return make_int_ag_inputs(M, N, K, c["n"], seed)
+    return make_int_rs_inputs(M, N, K, c["n"], seed)

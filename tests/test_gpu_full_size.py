@@ -1,10 +1,28 @@
-"""Parity at the full sizes of the evaluation workloads, in the launch
-configuration the benchmark times: fused operators on device-resident remote
-data, links unpaced at the copy engines' ceiling (configuration 5: its 4 : 1
-paced ring directions). The GPU computes the whole output; the oracle
-computes sampled rows (the first and last row of every partition plus seeded
-random rows), which cover every column tile, one row at a time through its
-own gather / GEMM / ReduceScatter code."""
+"""Parity at the full sizes of the evaluation workloads, every output element.
+
+Each case runs one operator at a configuration's exact full shape through the
+C ABI, in the launch configuration the benchmark times: fused operators (or
+InterDecom at every d of configuration 4) on device-resident remote data,
+links unpaced at the copy engines' ceiling, configuration 5 over its double
+ring with 4 : 1 paced directions. Two data sets per case:
+
+* ``int``: small-integer inputs (activations and weights in [-4, 4],
+  partials in [-64, 64]). Every fp32 partial sum is exact, so the whole bf16
+  output, and every chunk sent onward, must equal the oracle's exact result
+  rounded once to nearest-even, bit for bit.
+* ``seeded``: the configuration's seeded inputs (normal activations and
+  weights). Every element must lie within a rigorous bound of the fp64
+  oracle: one bf16 rounding of the accumulated value (unit roundoff 2^-8)
+  plus the worst-case fp32 accumulation error of K products and one partial
+  add (gamma_{K+1} with the unit 2^-23 of a faithful rounding, times the sum
+  of the terms' magnitudes); and the normwise relative error over the whole
+  output must stay below 5e-3.
+
+Every output, send and landing buffer is filled with NaN before the launch,
+so a tile the persistent scheduler skips, a row stored through a wrong map,
+or a remote row read before its arrival flag shows up as a non-finite or
+wrong element. The oracle computes the whole product in fp64 (a few seconds
+at these sizes)."""
 from __future__ import annotations
 
 import functools
@@ -15,208 +33,195 @@ import torch
 
 import oracle as O
 from paper_2609_10549_amd import compass as C
-from synth import make_config_inputs
-from tests.gpu_helpers import TOL, AGCase, RSCase, host_f64, rel_err
+from synth import CONFIGS, make_config_inputs, make_int_config_inputs
+from tests.gpu_helpers import TOL, AGCase, RSCase, host_bits, rel_err
 
 pytestmark = pytest.mark.gpu
 
 UNPACED = C.links(0.0, 0.0)
 LINKS_4_TO_1 = C.links(200e9, 50e9)
+BF16_NAN = 0x7FC0            # quiet NaN bit pattern, as int16
+U_BF16 = 2.0 ** -8           # bf16 unit roundoff (8 significant bits)
+U_ACC = 2.0 ** -23           # fp32 unit of a faithful (not necessarily nearest) rounding
 
 
 def _say(*a):
     print(*a, flush=True)
 
 
+@pytest.fixture(autouse=True)
+def _sync_after():
+    yield
+    C.compass_sync()
+    torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------ cases
+def _hops(n):
+    # the single ring with hops 3 -> 4 and 7 -> 0 at 50 GB/s, the rest at 200 GB/s
+    return [50e9 if q in (3, 7) else 200e9 for q in range(n)]
+
+
+# (id, config, pattern, ring, links, d (0: fused), rank)
+CASES = [
+    ("c2_ag_double", 2, "ag", "double", UNPACED, 0, 0),
+    ("c2_ag_double_sub4", 2, "ag", "double", C.links(0.0, 0.0, sub_chunks=4), 0, 0),
+    ("c2_ag_alltoall", 2, "ag", "alltoall", C.links(200e9, 50e9), 0, 0),
+    ("c2_ag_single_hops_rank3", 2, "ag", "single", C.links(200e9, hop_Bps=_hops(8)), 0, 3),
+    ("c3_rs_single", 3, "rs", "single", UNPACED, 0, 0),
+    ("c3_rs_single_sub4", 3, "rs", "single", C.links(0.0, 0.0, sub_chunks=4), 0, 0),
+    ("c4_ag_fused", 4, "ag", "single", UNPACED, 0, 0),
+    ("c4_ag_d1", 4, "ag", "single", UNPACED, 1, 0),
+    ("c4_ag_d2", 4, "ag", "single", UNPACED, 2, 0),
+    ("c4_ag_d4", 4, "ag", "single", UNPACED, 4, 0),
+    ("c4_ag_d8", 4, "ag", "single", UNPACED, 8, 0),
+    ("c4_ag_d16", 4, "ag", "single", UNPACED, 16, 0),
+    ("c5_ag_double_4to1", 5, "ag", "double", LINKS_4_TO_1, 0, 0),
+    ("c5_ag_split_4to1", 5, "ag", "double_split", LINKS_4_TO_1, 0, 0),
+    ("c5_rs_double_4to1", 5, "rs", "double", LINKS_4_TO_1, 0, 0),
+    ("c5_rs_split_4to1", 5, "rs", "double_split", LINKS_4_TO_1, 0, 0),
+    ("c5_rs_double_unpaced", 5, "rs", "double", UNPACED, 0, 0),
+]
+
+# cases sharing a reference are adjacent, so a cache of two holds them
+PARAMS = [pytest.param(kind, case, id=f"{case[0]}-{kind}") for case in CASES for kind in ("int", "seeded")]
+
+
 @functools.lru_cache(maxsize=2)
-def inputs(idx: int, pattern: str | None = None) -> dict:
-    return make_config_inputs(idx, pattern)
+def inputs(kind: str, idx: int, pattern: str) -> dict:
+    pat = pattern if idx == 5 else None
+    return make_int_config_inputs(idx, pat) if kind == "int" else make_config_inputs(idx, pat)
 
 
-def sample_rows(M: int, parts: int, seed: int, extra: int = 2) -> np.ndarray:
-    rng = np.random.default_rng(seed)
-    prow = M // parts
-    rows = []
-    for q in range(parts):
-        lo = q * prow
-        rows += [lo, lo + prow - 1] + list(rng.integers(lo, lo + prow, size=extra))
-    return np.unique(np.array(rows, dtype=np.int64))
+def _f64(bits):
+    return O.bf16_to_f64(bits)
 
 
-def device_rows(t: torch.Tensor, rows: np.ndarray) -> np.ndarray:
-    return host_f64(t.index_select(0, torch.from_numpy(rows).cuda()))
+@functools.lru_cache(maxsize=2)
+def reference(kind: str, idx: int, pattern: str, d: int):
+    """(exact fp64 result, elementwise bound or None) of the oracle."""
+    inp = inputs(kind, idx, pattern)
+    n, K = inp["n"], inp["K"]
+    if pattern == "ag":
+        sh = [_f64(s) for s in inp["shards"]]
+        W = _f64(inp["W"])
+        ref = O.decomp_ag(sh, W, d) if d >= 1 else O.ag_gemm(sh, W)
+        if kind == "int":
+            return ref, None
+        mag = np.abs(np.vstack(sh)) @ np.abs(W).T
+        terms = K
+    else:
+        A, W = _f64(inp["A"]), _f64(inp["W"])
+        P = [p.astype(np.float64) for p in inp["P_in"]]
+        ref = O.decomp_rs(A, W, P, n, d) if d >= 1 else O.gemm_rs(A, W, P, n)
+        if kind == "int":
+            return ref, None
+        mag = np.abs(A) @ np.abs(W).T + np.abs(np.vstack(P))
+        terms = K + 1
+    gamma = terms * U_ACC / (1.0 - terms * U_ACC)
+    err_acc = gamma * mag
+    bound = U_BF16 * np.abs(ref) + (1.0 + U_BF16) * err_acc
+    return ref, bound
 
 
-def ag_rows_reference(inp: dict, rows: np.ndarray) -> np.ndarray:
-    A = np.vstack(inp["shards"])[rows]
-    return O.ag_gemm([O.bf16_to_f64(A)], O.bf16_to_f64(inp["W"]))
-
-
-def rs_rows_reference(inp: dict, rows: np.ndarray) -> np.ndarray:
-    n, M = inp["n"], inp["M"]
-    prow = M // n
-    P = np.stack([inp["P_in"][r // prow][r % prow] for r in rows]).astype(np.float64)
-    return O.gemm_rs(O.bf16_to_f64(inp["A"][rows]), O.bf16_to_f64(inp["W"]), [P], 1)
-
-
-def split_boundary_rows(inp: dict, frac_bwd: float) -> np.ndarray:
-    """Rows on both sides of the candidate boundaries of a rate-proportional
-    split of every chunk (the exact share, and its roundings to 8 and to 128
-    rows)."""
-    rows = inp["M"] // inp["n"]
-    x = rows * frac_bwd
-    cands = {int(x), int(round(x / 8.0)) * 8, int(x // 128) * 128, -(-int(x) // 128) * 128}
-    return np.array(sorted({c * rows + h + o for c in range(inp["n"]) for h in cands for o in (-1, 0)
-                            if 0 < h < rows}), dtype=np.int64)
-
-
-def check_ag(case: AGCase, inp: dict, parts: int, seed: int, extra_rows=None):
-    torch.cuda.synchronize()
-    assert np.array_equal(case.gathered.cpu().numpy().view(np.uint16), np.vstack(inp["shards"]))
-    rows = sample_rows(inp["M"], parts, seed)
-    if extra_rows is not None:
-        rows = np.unique(np.concatenate([rows, extra_rows]))
-    got = device_rows(case.C, rows)
-    assert np.isfinite(got).all()
-    err = rel_err(got, ag_rows_reference(inp, rows))
-    _say("rows", len(rows), "normwise rel. error", err)
-    assert err < TOL
-
-
-def check_rs(case: RSCase, inp: dict, parts: int, seed: int, extra_rows=None):
-    torch.cuda.synchronize()
-    rows = sample_rows(inp["M"], parts, seed)
-    if extra_rows is not None:
-        rows = np.unique(np.concatenate([rows, extra_rows]))
-    got = device_rows(case.C, rows)
-    assert np.isfinite(got).all()
-    err = rel_err(got, rs_rows_reference(inp, rows))
-    _say("rows", len(rows), "normwise rel. error", err)
-    assert err < TOL
-    # every chunk sum sent onward equals the stored one
-    prow = inp["M"] // inp["n"]
-    for q, s in enumerate(case.send):
-        if s is None:
+def _nan_fill(*tensors):
+    for t in tensors:
+        if t is None:
             continue
-        assert torch.equal(s, case.C[q * prow:(q + 1) * prow]), q
+        if t.dtype == torch.int16:
+            t.fill_(BF16_NAN)
+        else:
+            t.fill_(float("nan"))
 
 
-def test_config2_fused_allgather_full_size():
-    inp = inputs(2)
-    case = AGCase(inp, 0, "double")
-    _say("config 2: fused AllGather", inp["M"], inp["N"], inp["K"])
-    C.compass_ag_gemm(case.problem, UNPACED)
-    C.compass_sync()
-    check_ag(case, inp, 2 * inp["n"], seed=201)
+def _compare(name: str, got_bits: np.ndarray, ref: np.ndarray, bound, kind: str):
+    if kind == "int":
+        want = O.f64_to_bf16_rne(ref)
+        bad = got_bits != want
+        nbad = int(bad.sum())
+        if nbad:
+            r, c = np.argwhere(bad)[0]
+            _say(f"{name}: {nbad} of {bad.size} elements differ; first at ({r}, {c}): "
+                 f"got {got_bits[r, c]:#06x}, want {want[r, c]:#06x}")
+        assert nbad == 0, name
+        _say(f"{name}: {got_bits.size} elements bit-exact")
+        return
+    got = O.bf16_to_f64(got_bits)
+    finite = np.isfinite(got)
+    assert finite.all(), f"{name}: {int((~finite).sum())} non-finite elements"
+    excess = np.abs(got - ref) - bound
+    nbad = int((excess > 0).sum())
+    if nbad:
+        r, c = np.unravel_index(int(np.argmax(excess)), excess.shape)
+        _say(f"{name}: {nbad} elements outside the bound; worst at ({r}, {c}): got {got[r, c]}, "
+             f"oracle {ref[r, c]}, bound {bound[r, c]}")
+    assert nbad == 0, name
+    err = rel_err(got, ref)
+    ratio = float(np.max(np.abs(got - ref) / np.maximum(bound, 1e-300)))
+    _say(f"{name}: {got_bits.size} elements within the bound (largest error / bound {ratio:.3f}), "
+         f"normwise relative error {err:.3e}")
+    assert err < TOL, name
 
 
-def test_config3_fused_reducescatter_full_size():
-    inp = inputs(3)
-    case = RSCase(inp, 0, "single")
-    _say("config 3: fused ReduceScatter", inp["M"], inp["N"], inp["K"])
-    C.compass_gemm_rs(case.problem, UNPACED)
-    C.compass_sync()
-    check_rs(case, inp, inp["n"], seed=301)
-
-
-@pytest.mark.parametrize("d", [0, 1, 2, 4, 8, 16])
-def test_config4_interdecom_full_size(d):
-    # d = 0: the fused operator on the same workload
-    inp = inputs(4)
-    case = AGCase(inp, 0, "single")
-    _say("config 4: d =", d)
-    if d == 0:
-        C.compass_ag_gemm(case.problem, UNPACED)
-    else:
-        C.compass_decomp_gemm(case.problem, d, UNPACED)
-    C.compass_sync()
-    check_ag(case, inp, inp["n"], seed=400 + d)
-
-
-@pytest.mark.parametrize("pattern", ["ag", "rs"])
-def test_config5_double_ring_4_to_1_full_size(pattern):
-    inp = inputs(5, pattern)
-    _say("config 5:", pattern, inp["M"], inp["N"], inp["K"])
+@pytest.mark.parametrize("kind,case", PARAMS)
+def test_full_size_every_element(kind, case):
+    cid, idx, pattern, ring, lk, d, rank = case
+    inp = inputs(kind, idx, pattern)
+    M, N, K, n = inp["M"], inp["N"], inp["K"], inp["n"]
+    _say(f"full size {cid} [{kind}]: {pattern} M={M} N={N} K={K} n={n} ring={ring} d={d} rank={rank} "
+         f"rates={lk.fwd_Bps:.3g}/{lk.bwd_Bps:.3g} sub={lk.sub_chunks}")
+    trace = cid == "c5_rs_double_unpaced"
     if pattern == "ag":
-        case = AGCase(inp, 0, "double")
-        C.compass_ag_gemm(case.problem, LINKS_4_TO_1)
+        case_ = AGCase(inp, rank, ring)
+        rows = M // n
+        keep = case_.gathered[rank * rows:(rank + 1) * rows].clone()
+        _nan_fill(case_.gathered, case_.C)
+        case_.gathered[rank * rows:(rank + 1) * rows] = keep
+        del keep
+        torch.cuda.synchronize()
+        if d == 0:
+            C.compass_ag_gemm(case_.problem, lk)
+        else:
+            C.compass_decomp_gemm(case_.problem, d, lk)
         C.compass_sync()
-        check_ag(case, inp, 2 * inp["n"], seed=501)
+        torch.cuda.synchronize()
+        # the gathered input is the shards stacked in rank order, bit for bit
+        assert np.array_equal(host_bits(case_.gathered), np.vstack(inp["shards"]))
     else:
-        case = RSCase(inp, 0, "double")
-        C.compass_gemm_rs(case.problem, LINKS_4_TO_1)
-        C.compass_sync()
-        check_rs(case, inp, 2 * inp["n"], seed=502)
+        case_ = RSCase(inp, rank, ring)
+        _nan_fill(case_.C, case_.stage, *(case_.send or []))
+        torch.cuda.synchronize()
+        if trace:
+            C.compass_set_option(C.OPT_TILE_TRACE, 8192)
+        try:
+            if d == 0:
+                C.compass_gemm_rs(case_.problem, lk)
+            else:
+                C.compass_decomp_gemm(case_.problem, d, lk)
+            C.compass_sync()
+            torch.cuda.synchronize()
+            if trace:
+                # unpaced links make the GPT-3 ReduceScatter computation-
+                # dominated (estimated lambda > 1): it takes 256 x 256 tiles,
+                # one trace record per output tile
+                rec = C.compass_tile_trace(8192)
+                assert len(rec) == (M // 256) * (N // 256)
+        finally:
+            if trace:
+                C.compass_set_option(C.OPT_TILE_TRACE, 0)
+        # every chunk sum sent onward equals the stored one, bit for bit
+        prow = M // n
+        for q, s in enumerate(case_.send):
+            if s is not None:
+                assert torch.equal(s, case_.C[q * prow:(q + 1) * prow]), f"send {q}"
+    got = host_bits(case_.C)
+    del case_
+    ref, bound = reference(kind, idx, pattern, d)
+    _compare(f"{cid} [{kind}]", got, ref, bound, kind)
 
 
-def test_config5_reducescatter_unpaced_takes_256_tiles():
-    # Unpaced links make the GPT-3 ReduceScatter computation-dominated
-    # (estimated lambda > 1), where the operator takes 256 x 256 tiles: the
-    # tile trace holds one record per output tile, 32 x 48 of them.
-    inp = inputs(5, "rs")
-    case = RSCase(inp, 0, "double")
-    _say("config 5: rs unpaced, tile trace")
-    C.compass_set_option(C.OPT_TILE_TRACE, 8192)
-    try:
-        C.compass_gemm_rs(case.problem, UNPACED)
-        C.compass_sync()
-        rec = C.compass_tile_trace(8192)
-    finally:
-        C.compass_set_option(C.OPT_TILE_TRACE, 0)
-    assert len(rec) == (inp["M"] // 256) * (inp["N"] // 256)
-    check_rs(case, inp, 2 * inp["n"], seed=503)
-
-
-@pytest.mark.parametrize("pattern", ["ag", "rs"])
-def test_config5_proportional_double_ring_4_to_1_full_size(pattern):
-    # the same workload with each chunk's rows split 1 : 4 between the rings
-    inp = inputs(5, pattern)
-    _say("config 5 split:", pattern)
-    if pattern == "ag":
-        case = AGCase(inp, 0, "double_split")
-        C.compass_ag_gemm(case.problem, LINKS_4_TO_1)
-        C.compass_sync()
-        check_ag(case, inp, 2 * inp["n"], seed=511, extra_rows=split_boundary_rows(inp, 0.2))
-    else:
-        case = RSCase(inp, 0, "double_split")
-        C.compass_gemm_rs(case.problem, LINKS_4_TO_1)
-        C.compass_sync()
-        check_rs(case, inp, 2 * inp["n"], seed=512, extra_rows=split_boundary_rows(inp, 0.2))
-
-
-@pytest.mark.parametrize("ring", ["alltoall", "single_hops"])
-def test_config2_cross_numa_links_full_size(ring):
-    # the fc1 workload over the cross-NUMA link patterns: AlltoAll (own
-    # domain 200 GB/s, 50 GB/s shared across) and the single ring with hops
-    # 3 -> 4 and 7 -> 0 at 50 GB/s, the rest at 200 GB/s (rank 3)
-    inp = inputs(2)
-    _say("config 2 cross-NUMA:", ring)
-    if ring == "alltoall":
-        case, lk = AGCase(inp, 0, "alltoall"), C.links(200e9, 50e9)
-    else:
-        hops = [50e9 if q in (3, 7) else 200e9 for q in range(inp["n"])]
-        case, lk = AGCase(inp, 3, "single"), C.links(200e9, hop_Bps=hops)
-    C.compass_ag_gemm(case.problem, lk)
-    C.compass_sync()
-    check_ag(case, inp, inp["n"], seed=521)
-
-
-@pytest.mark.parametrize("pattern", ["ag", "rs"])
-def test_config2_config3_sub_chunk_flags_full_size(pattern):
-    # the benchmark's two operators with four arrival flags per partition
-    # (128-row pieces for the AllGather's 512-row partitions)
-    lk = C.links(0.0, 0.0, sub_chunks=4)
-    if pattern == "ag":
-        inp = inputs(2)
-        case = AGCase(inp, 0, "double")
-        _say("config 2 sub-chunks")
-        C.compass_ag_gemm(case.problem, lk)
-        C.compass_sync()
-        check_ag(case, inp, 8 * inp["n"], seed=531)
-    else:
-        inp = inputs(3)
-        case = RSCase(inp, 0, "single")
-        _say("config 3 sub-chunks")
-        C.compass_gemm_rs(case.problem, lk)
-        C.compass_sync()
-        check_rs(case, inp, 4 * inp["n"], seed=532)
+def test_config_table_matches_the_cases():
+    # every full-size configuration (2-5) and both configuration-5 patterns appear above
+    seen = {(c[1], c[2]) for c in CASES}
+    assert seen == {(2, "ag"), (3, "rs"), (4, "ag"), (5, "ag"), (5, "rs")}
+    assert {c[5] for c in CASES if c[1] == 4} == {0, *CONFIGS[4]["d_list"]}
