@@ -641,10 +641,21 @@ def fusion_m(pattern: str, M: int, N: int, K: int) -> float:
 
 
 def select_strategy(t_fus: float, t_dec: float):
-    """Algorithm 1, phase 3: TA-IntraFusion when its predicted time is
-    strictly lower, ODP-InterDecom otherwise; T* is the minimum."""
+    """Eq. 6: the strategy with the lower predicted time, TA-IntraFusion only
+    when strictly lower (a tie keeps ODP-InterDecom, as the selection
+    algorithm of Section V-C states); returns it with that time."""
     s = "intra_fusion" if t_fus < t_dec else "inter_decom"
     return s, min(t_fus, t_dec)
+
+
+def feasible_degree(chunk_rows: int, d_max: int) -> int:
+    """Largest power of two d <= d_max whose sub-operators split a chunk's
+    rows evenly (every sub-operator takes chunk_rows / d rows of each
+    chunk)."""
+    d = 1
+    while d * 2 <= d_max and chunk_rows % (d * 2) == 0:
+        d *= 2
+    return d
 
 
 def pick_strategy(pattern: str, ring: str, M: int, N: int, K: int, n: int,
@@ -652,29 +663,25 @@ def pick_strategy(pattern: str, ring: str, M: int, N: int, K: int, n: int,
                   a_c: float, b_c: float, alpha_d: float, beta_d: float,
                   alpha_f: float, beta_f: float, d_max: int = 16,
                   literal: bool = False) -> dict:
-    """Algorithm 1 end to end (Eq. 2-8): base times, lambda, d*, both
-    predicted times and the chosen strategy. d* is additionally limited to
-    degrees that split every chunk's rows evenly (largest power of two not
-    above the candidate)."""
+    """Strategy selection of Section V (Algorithm 1) from its models: the
+    calibrated base times, ODP-InterDecom's predicted time at the degree of
+    Eq. 4-5 (limited to degrees that split every chunk's rows evenly), and
+    TA-IntraFusion's predicted time by Eq. 7-8 with one chunk of computation
+    Tc/n against one ring step of communication; the lower one wins
+    (Eq. 6)."""
     Tc = t_comp(M, N, K, a_c, b_c)
     Tm = t_comm(pattern, ring, M, N, K, n, fwd_Bps, bwd_Bps, tau)
-    lam = Tc / Tm
-    rows = M // n
-    feas = 1
-    while feas * 2 <= d_max and rows % (feas * 2) == 0:
-        feas *= 2
-    dmax_eff = feas
-    dc = d_candidate(lam, alpha_d, beta_d, dmax_eff, literal)
-    d_star = dc if t_decomp(Tc, Tm, dc, alpha_d, beta_d) < t_decomp(Tc, Tm, 1, alpha_d, beta_d) else 1
+    d_cap = feasible_degree(M // n, d_max)
+    dc = d_candidate(Tc / Tm, alpha_d, beta_d, d_cap, literal)
+    d_star = d_final(Tc, Tm, alpha_d, beta_d, d_cap, literal)
     Tdec = t_decomp(Tc, Tm, d_star, alpha_d, beta_d)
-    Tdec1 = t_decomp(Tc, Tm, 1, alpha_d, beta_d)
     step_comm = Tm / (n - 1) if n > 1 else 0.0
     comp_chunks = [Tc / n] * n
     comm_chunks = [0.0] + [step_comm] * (n - 1)
     Tfus = t_fusion(comp_chunks, comm_chunks, alpha_f, beta_f, fusion_m(pattern, M, N, K))
     s, T = select_strategy(Tfus, Tdec)
-    return dict(strategy=s, t_star=T, d_star=d_star, d_cand=dc, lam=lam, t_comp=Tc,
-                t_comm=Tm, t_fusion=Tfus, t_decomp=Tdec, t_decomp1=Tdec1)
+    return dict(strategy=s, t_star=T, d_star=d_star, d_cand=dc, lam=Tc / Tm, t_comp=Tc,
+                t_comm=Tm, t_fusion=Tfus, t_decomp=Tdec, t_decomp1=t_decomp(Tc, Tm, 1, alpha_d, beta_d))
 
 
 # --------------------------------------------------------------------------

@@ -2,6 +2,7 @@
 // (Section III-A/B), the InterDecom and IntraFusion time models (Eq. 2-8),
 // the strategy selector (Algorithm 1) and the calibration fits
 // (Section IV-C). Everything is fp64 and O(1) per call.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <vector>
@@ -171,6 +172,33 @@ double model_t_fusion(const compass_workload &w, double tc, double tm_step, doub
     return body + c + (n - 1) * (af + bf * m);
 }
 
+// Degree of ODP-InterDecom (Section IV-C) for base times tc, tm: the
+// stationary point of Eq. 2 in d rounded to a power of two (Eq. 5), capped at
+// d_max and at the largest power of two that splits a chunk's rows evenly,
+// kept only when its predicted time beats the undecomposed operator (Eq. 4).
+struct Degree {
+    int cand, best;         // Eq. 5 candidate, chosen degree
+    double t_best, t_one;   // Eq. 2 at the chosen degree and at d = 1
+};
+
+static Degree optimal_degree(double tc, double tm, int chunk_rows, const compass_calib &cal) {
+    int feasible = 1;
+    while (feasible * 2 <= cal.d_max && chunk_rows % (feasible * 2) == 0) feasible *= 2;
+    const double x = d_stationary(tc / tm, cal.alpha_decomp, cal.beta_decomp, cal.literal_eq5);
+    Degree g;
+    g.cand = std::isinf(x) ? feasible : std::min(std::max(p2_round(x), 1), feasible);
+    g.t_one = model_t_decomp(tc, tm, 1, cal.alpha_decomp, cal.beta_decomp);
+    const double t_cand = model_t_decomp(tc, tm, g.cand, cal.alpha_decomp, cal.beta_decomp);
+    g.best = t_cand < g.t_one ? g.cand : 1;
+    g.t_best = g.best == g.cand ? t_cand : g.t_one;
+    return g;
+}
+
+// Strategy selection of Section V (the problem of Eq. 6, solved in O(1) by
+// the selection algorithm, Algorithm 1): predict the operator time of
+// ODP-InterDecom at its degree (Eq. 2-5) and of TA-IntraFusion (Eq. 7-8,
+// chunk computation Tc / n against one ring step of communication), both from
+// the calibrated base times, and take the lower; a tie goes to InterDecom.
 int pick(const compass_workload *w, const compass_topology *t, const compass_calib *cal,
          compass_choice *out) {
     if (!w || !t || !cal || !out) return set_error(COMPASS_ERR_INVALID, "pick_strategy: null argument");
@@ -185,36 +213,22 @@ int pick(const compass_workload *w, const compass_topology *t, const compass_cal
     if (!(t->fwd_Bps > 0) || (t->ring != COMPASS_RING_SINGLE && !(t->bwd_Bps > 0)))
         return set_error(COMPASS_ERR_INVALID, "pick_strategy: link rates must be positive");
     if (cal->d_max < 1) return set_error(COMPASS_ERR_INVALID, "pick_strategy: d_max < 1");
-    // Phase 1: base metrics
     const double tc = model_t_comp(*w, *cal);
     const double tm = model_t_comm(*w, *t);
     if (!(tc > 0) || !(tm > 0)) return set_error(COMPASS_ERR_INVALID, "pick_strategy: non-positive base time");
-    const double lam = tc / tm;
-    // Phase 2: degree (Eq. 5 then Eq. 4), limited to even splits of a chunk
-    const int rows = w->M / w->n;
-    int feas = 1;
-    while (feas * 2 <= cal->d_max && rows % (feas * 2) == 0) feas *= 2;
-    const double x = d_stationary(lam, cal->alpha_decomp, cal->beta_decomp, cal->literal_eq5);
-    int dc = std::isinf(x) ? feas : p2_round(x);
-    if (dc > feas) dc = feas;
-    if (dc < 1) dc = 1;
-    const double t1 = model_t_decomp(tc, tm, 1, cal->alpha_decomp, cal->beta_decomp);
-    const double tdc = model_t_decomp(tc, tm, dc, cal->alpha_decomp, cal->beta_decomp);
-    const int dstar = tdc < t1 ? dc : 1;
-    const double tdec = dstar == dc ? tdc : t1;
-    // Phase 3: both predictions and the choice
+    const Degree dg = optimal_degree(tc, tm, w->M / w->n, *cal);
     const double step = w->n > 1 ? tm / (w->n - 1) : 0.0;
     const double tfus = model_t_fusion(*w, tc, step, cal->alpha_fusion, cal->beta_fusion);
-    out->strategy = tfus < tdec ? COMPASS_INTRA_FUSION : COMPASS_INTER_DECOM;
-    out->t_star = std::fmin(tfus, tdec);
-    out->d_star = dstar;
-    out->d_cand = dc;
-    out->lambda = lam;
+    out->strategy = tfus < dg.t_best ? COMPASS_INTRA_FUSION : COMPASS_INTER_DECOM;
+    out->t_star = std::fmin(tfus, dg.t_best);
+    out->d_star = dg.best;
+    out->d_cand = dg.cand;
+    out->lambda = tc / tm;
     out->t_comp = tc;
     out->t_comm = tm;
     out->t_fusion = tfus;
-    out->t_decomp = tdec;
-    out->t_decomp1 = t1;
+    out->t_decomp = dg.t_best;
+    out->t_decomp1 = dg.t_one;
     return COMPASS_OK;
 }
 
