@@ -50,6 +50,12 @@ extern "C" {
 #define COMPASS_ERR_UNSUPPORTED -2  /* valid but outside what is implemented  */
 #define COMPASS_ERR_HIP         -3  /* HIP / HSA runtime call failed          */
 #define COMPASS_ERR_TIMEOUT     -4  /* a bounded wait (flag, copy) expired    */
+#define COMPASS_ERR_IN_FLIGHT   -5  /* copies of a failed job were still running
+                                       when the copy side gave up waiting for
+                                       them: they may still write caller
+                                       buffers, so every later call is refused
+                                       with this status (the process must not
+                                       free or reuse those buffers)          */
 
 /* ---- enumerations ------------------------------------------------------ */
 #define COMPASS_AG_GEMM   0  /* AllGather + GEMM      (Section II-A, Fig. 1) */
@@ -268,7 +274,8 @@ int compass_sequential(const compass_problem *p, const compass_links *links, voi
 
 /* Wait until the copy side of every enqueued operator has finished and the
  * device is idle; return the pending asynchronous status (COMPASS_OK or
- * COMPASS_ERR_TIMEOUT) and clear it. */
+ * COMPASS_ERR_TIMEOUT) and clear it. COMPASS_ERR_IN_FLIGHT (not cleared) when
+ * a failed job's copies did not land within the host-side bound. */
 int compass_sync(void);
 
 /* ---- tuning / test options -------------------------------------------- */

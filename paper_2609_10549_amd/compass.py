@@ -19,6 +19,7 @@ ERR_INVALID = -1
 ERR_UNSUPPORTED = -2
 ERR_HIP = -3
 ERR_TIMEOUT = -4
+ERR_IN_FLIGHT = -5
 
 AG_GEMM = 0
 GEMM_RS = 1
@@ -190,12 +191,38 @@ class Problem:
         self._keep = keep
 
 
+def _shape_of(x):
+    return tuple(int(v) for v in x.shape)
+
+
+def _need(x, what: str, shape: tuple, elsize: int) -> None:
+    """Raise ValueError unless tensor x is contiguous with the given shape and
+    element size (the library takes raw addresses and derives every extent
+    from M, N, K and n, so a mismatch would send its copies and loads outside
+    the tensor). Plain int addresses are the caller's responsibility."""
+    if x is None or isinstance(x, int):
+        return
+    if _shape_of(x) != tuple(shape):
+        raise ValueError(f"{what}: shape {_shape_of(x)}, expected {tuple(shape)}")
+    if x.element_size() != elsize:
+        raise ValueError(f"{what}: element size {x.element_size()} bytes, expected {elsize}")
+    if not x.is_contiguous():
+        raise ValueError(f"{what}: must be contiguous")
+
+
 def ag_problem(shards: Sequence, gathered, W, C, rank: int, ring: str | int = "double") -> Problem:
     """AllGather+GEMM operands: n shards (M/n x K bf16), gathered (M x K),
     W (N x K), C (M x N). Tensors hold bf16 values (dtype bfloat16 or int16)."""
     n = len(shards)
     M, K = gathered.shape
     N = W.shape[0]
+    if n < 1 or M % n:
+        raise ValueError(f"M = {M} rows must split into n = {n} shards")
+    _need(gathered, "gathered", (M, K), 2)
+    _need(W, "W", (N, K), 2)
+    _need(C, "C", (M, N), 2)
+    for q, sh in enumerate(shards):
+        _need(sh, f"shards[{q}]", (M // n, K), 2)
     arr = _ptr_array(shards)
     st = compass_problem(pattern=AG_GEMM, M=M, N=N, K=K, n=n, rank=rank,
                          ring=RINGS.get(ring, ring), W=_addr(W), C=_addr(C),
@@ -211,6 +238,19 @@ def rs_problem(A, W, partial_src: Sequence, partial_stage, C, send_dst: Sequence
     n = len(partial_src)
     M, K = A.shape
     N = W.shape[0]
+    if n < 1 or M % n:
+        raise ValueError(f"M = {M} rows must split into n = {n} chunks")
+    _need(A, "A", (M, K), 2)
+    _need(W, "W", (N, K), 2)
+    _need(C, "C", (M, N), 2)
+    _need(partial_stage, "partial_stage", (M, N), 4)
+    for q, p in enumerate(partial_src):
+        _need(p, f"partial_src[{q}]", (M // n, N), 4)
+    if send_dst is not None:
+        if len(send_dst) != n:
+            raise ValueError(f"send_dst: {len(send_dst)} entries, expected {n}")
+        for q, x in enumerate(send_dst):
+            _need(x, f"send_dst[{q}]", (M // n, N), 2)
     parr = _ptr_array(partial_src)
     sarr = None
     if send_dst is not None:
@@ -263,6 +303,10 @@ def compass_decomp_gemm(problem: Problem, d: int, lk: compass_links | None = Non
 def compass_gemm(A, W, C, P=None, stream=None) -> None:
     M, K = A.shape
     N = W.shape[0]
+    _need(A, "A", (M, K), 2)
+    _need(W, "W", (N, K), 2)
+    _need(C, "C", (M, N), 2)
+    _need(P, "P", (M, N), 4)
     _check(lib().compass_gemm(M, N, K, _addr(A), _addr(W), _addr(C), _addr(P), _stream(stream)), "compass_gemm")
 
 

@@ -142,8 +142,8 @@ struct Pacer {
     void loop();
     void execute(Job &job);
     void execute_pooled(Job &job);
-    hsa_signal_t take_signal();
-    void quiesce();
+    bool take_signal(hsa_signal_t *out);
+    bool quiesce();
 };
 
 struct Ctx {
@@ -158,6 +158,7 @@ struct Ctx {
     uint32_t epoch = 0;
     Pacer pacer[kRoles];
     std::atomic<int> async_err{0};
+    std::atomic<bool> in_flight{false};   // a failed job's copies outlived the bound
     uint32_t spin_limit = 4u << 20;  // kernel polls (about 0.5 us each)
     double host_timeout = 5.0;       // seconds
     int grid_override = 0;
@@ -376,29 +377,38 @@ static int agent_of(const void *ptr, hsa_agent_t *out) {
 }
 
 // ---------------------------------------------------------------- pacer
-hsa_signal_t Pacer::take_signal() {
+// The next completion signal, armed with 1 for a new copy. A slot comes
+// round again kSignals copies later: if the copy it tracked has not landed
+// within the host-side bound, the slot is left as it is (re-armed, the old
+// copy's completion would count as the new copy's landing) and false is
+// returned, so that the caller issues nothing and the job ends on the error.
+bool Pacer::take_signal(hsa_signal_t *out) {
     hsa_signal_t s = sig[sig_next];
-    sig_next = (sig_next + 1) % kSignals;
-    // a slot is reused kSignals copies later; make sure that copy finished
     const double t0 = now_s();
     while (hsa_signal_load_scacquire(s) > 0) {
-        if (now_s() - t0 > ctx->host_timeout) { ctx->async_err.store(COMPASS_ERR_TIMEOUT); break; }
+        if (now_s() - t0 > ctx->host_timeout) {
+            ctx->async_err.store(COMPASS_ERR_TIMEOUT);
+            return false;
+        }
         _mm_pause();
     }
+    sig_next = (sig_next + 1) % kSignals;
     hsa_signal_store_relaxed(s, 1);
-    return s;
+    *out = s;
+    return true;
 }
 
 // Wait until every copy issued with this pacer's signals has completed
 // (bounded: the host timeout, at least one second, since the timeout may be
-// what ended the job).
-void Pacer::quiesce() {
+// what ended the job). False when copies were still in flight at the bound.
+bool Pacer::quiesce() {
     const double t0 = now_s(), bound = std::max(1.0, ctx->host_timeout);
     for (int i = 0; i < kSignals; ++i)
         while (hsa_signal_load_scacquire(sig[i]) > 0) {
-            if (now_s() - t0 > bound) return;
+            if (now_s() - t0 > bound) return false;
             _mm_pause();
         }
+    return true;
 }
 
 void Pacer::loop() {
@@ -424,7 +434,9 @@ void Pacer::loop() {
         // a job that ended on an error may have left copies in flight: let them
         // land before the job counts as done, so that compass_sync() returns
         // with none of them still writing the caller's buffers
-        if (ctx->async_err.load() != 0) quiesce();
+        // (copies that outlive the bound leave the library refusing every
+        // later call: they may still write the caller's buffers)
+        if (ctx->async_err.load() != 0 && !quiesce()) ctx->in_flight.store(true);
         pending.fetch_sub(1, std::memory_order_acq_rel);
         idle_since = now_s();
     }
@@ -528,7 +540,8 @@ void Pacer::execute(Job &job) {
     double gate_time = 0;
 
     auto issue = [&](const Item &it, size_t o, size_t len, size_t e) -> bool {
-        hsa_signal_t sg = take_signal();
+        hsa_signal_t sg;
+        if (!take_signal(&sg)) return false;
         const hsa_status_t st = hsa_amd_memory_async_copy_on_engine(
             (char *)it.dst + o, it.dst_agent, (const char *)it.src + o, it.src_agent, len, 0, nullptr, sg,
             (hsa_amd_sdma_engine_id_t)job.engines[e], true);
@@ -740,7 +753,8 @@ void Pacer::execute_pooled(Job &job) {
             const Item &it = job.items[pick];
             State &s = st[pick];
             const size_t len = std::min(s.per, it.bytes - s.off);
-            hsa_signal_t sg = take_signal();
+            hsa_signal_t sg;
+            if (!take_signal(&sg)) return;
             const hsa_status_t rc = hsa_amd_memory_async_copy_on_engine(
                 (char *)it.dst + s.off, it.dst_agent, (const char *)it.src + s.off, it.src_agent, len, 0, nullptr, sg,
                 (hsa_amd_sdma_engine_id_t)job.engines[e], true);
@@ -792,6 +806,9 @@ static bool pacers_idle() {
 // ---------------------------------------------------------------- helpers
 static int take_async_error() {
     Ctx &c = g_ctx;
+    if (c.in_flight.load())
+        return set_error(COMPASS_ERR_IN_FLIGHT, "copies of a failed transfer job outlived the host-side bound and may "
+                                                "still write the caller's buffers; the library refuses further calls");
     const int a = c.async_err.exchange(0);
     const uint32_t k = __atomic_exchange_n(&c.hw[kHwErr], 0u, __ATOMIC_ACQ_REL);
     if (k != 0) return set_error(COMPASS_ERR_TIMEOUT, "a kernel-side wait exceeded its bound (code %u)", k);
@@ -803,32 +820,88 @@ static int take_async_error() {
 static uint32_t next_epoch() { return ++g_ctx.epoch; }
 
 // SDMA engines of one ring direction: the usable engines are split over the
-// directions active in the operator in proportion to the bytes each carries
-// (`active` lists their roles, `weight` their relative traffic).
-static std::vector<uint32_t> engines_for(int role, const std::vector<int> &active, const std::vector<int> &weight,
-                                         int per_ring) {
+// directions active in the operator in proportion to `weight` (`active`
+// lists their roles): the bytes each carries, times its rate when the
+// directions are paced at different rates (a link four times faster needs
+// four times the copy throughput while it runs). Unequal shares go in whole
+// pairs of engines, so that a paced direction can group its engines (a group
+// width divides the count: 13 engines would leave only groups of 1 or 13),
+// with every direction keeping at least one pair; equal-rate splits keep
+// their plain proportional ranges.
+static std::vector<uint32_t> engines_for(int role, const std::vector<int> &active, const std::vector<double> &weight,
+                                         int per_ring, bool paired = false) {
     std::vector<uint32_t> all;
     for (uint32_t e : g_ctx.engines)
         if (g_ctx.engine_mask == 0 || (g_ctx.engine_mask & e)) all.push_back(e);
     if (all.empty()) all = g_ctx.engines;
     const int n = (int)all.size();
     const int na = std::max<int>(1, (int)active.size());
-    int wsum = 0;
+    double wsum = 0;
     for (int i = 0; i < na; ++i) wsum += weight[i];
     int first = 0, count = 1;
-    for (int i = 0, acc = 0; i < na; ++i) {
-        const int lo = (int)((long)n * acc / wsum);
-        acc += weight[i];
-        const int hi = (int)((long)n * acc / wsum);
-        if (active[i] == role) {
-            first = lo;
-            count = std::max(1, hi - lo);
+    if (paired && n >= 2 * na) {
+        // largest-remainder apportionment of n / 2 pairs, at least one each
+        const int units = n / 2;
+        std::vector<int> cnt(na);
+        std::vector<double> rem(na);
+        int used = 0;
+        for (int i = 0; i < na; ++i) {
+            const double ideal = units * weight[i] / wsum;
+            cnt[i] = std::max(1, (int)std::floor(ideal));
+            rem[i] = ideal - std::floor(ideal);
+            used += cnt[i];
+        }
+        while (used > units) {   // a forced pair came out of the largest share
+            const int big = (int)(std::max_element(cnt.begin(), cnt.end()) - cnt.begin());
+            --cnt[big];
+            --used;
+        }
+        while (used < units) {
+            const int r = (int)(std::max_element(rem.begin(), rem.end()) - rem.begin());
+            ++cnt[r];
+            rem[r] = -1.0;
+            ++used;
+        }
+        for (int i = 0, acc = 0; i < na; ++i) {
+            const int c = 2 * cnt[i] + (i == na - 1 ? n - 2 * units : 0);
+            if (active[i] == role) {
+                first = acc;
+                count = c;
+            }
+            acc += c;
+        }
+    } else {
+        double acc = 0;
+        for (int i = 0; i < na; ++i) {
+            const int lo = (int)((double)n * acc / wsum);
+            acc += weight[i];
+            const int hi = (int)((double)n * acc / wsum);
+            if (active[i] == role) {
+                first = lo;
+                count = std::max(1, hi - lo);
+            }
         }
     }
     if (per_ring > 0) count = std::min(count, per_ring);
     std::vector<uint32_t> out;
     for (int i = 0; i < count; ++i) out.push_back(all[(first + i) % n]);
     return out;
+}
+
+// Engine weights of the active directions: `bytes` (their relative traffic),
+// times the direction's rate when all of them are paced and the two ring
+// directions' rates differ (roles 0 and 2 run at the forward rate, 1 and 3
+// at the backward one). Returns whether the rates entered.
+static bool direction_weights(const std::vector<int> &active, const std::vector<int> &bytes, const compass_links *l,
+                              std::vector<double> *out) {
+    out->assign(bytes.begin(), bytes.end());
+    const bool by_rate = l->fwd_Bps > 0 && l->bwd_Bps > 0 && l->fwd_Bps != l->bwd_Bps && !l->hop_Bps;
+    if (!by_rate) return false;
+    bool both = false;
+    for (int r : active) both |= r % 2 == 1;
+    if (!both) return false;
+    for (size_t i = 0; i < active.size(); ++i) (*out)[i] *= active[i] % 2 == 0 ? l->fwd_Bps : l->bwd_Bps;
+    return true;
 }
 
 // The paper's double ring in either split (two partitions per chunk).
@@ -1210,12 +1283,12 @@ static int make_item(Item *it, void *dst, const void *src, size_t bytes, int fla
 }
 
 static void fill_job(Job &j, const compass_links *l, bool fwd, uint32_t epoch, int role, const std::vector<int> &active,
-                     const std::vector<int> &weight) {
+                     const std::vector<double> &weight, bool paired) {
     j.rate = fwd ? l->fwd_Bps : l->bwd_Bps;
     j.slice = l->slice_bytes ? l->slice_bytes : kDefaultSlice;
     j.slice_default = l->slice_bytes == 0;
     j.epoch = epoch;
-    j.engines = engines_for(role, active, weight, l->engines_per_ring);
+    j.engines = engines_for(role, active, weight, l->engines_per_ring, paired);
 }
 
 // Per-hop rates: the due times of the d * (n - 1) items this rank receives
@@ -1241,9 +1314,12 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
     const std::vector<int> active = p->ring == COMPASS_RING_SINGLE ? std::vector<int>{0} : std::vector<int>{0, 1};
     // AlltoAll: role 0 carries the dom - 1 chunks of this rank's domain, role 1
     // the dom chunks of the other domain
-    const std::vector<int> weight = a2a ? std::vector<int>{std::max(1, dom - 1), dom} : std::vector<int>(active.size(), 1);
-    fill_job(*fwd, l, true, epoch, 0, active, weight);
-    fill_job(*bwd, l, false, epoch, 1, active, weight);
+    const std::vector<int> bytes = a2a ? std::vector<int>{std::max(1, dom - 1), dom} : std::vector<int>(active.size(), 1);
+    std::vector<double> weight;
+    const bool paired = !a2a && direction_weights(active, bytes, l, &weight);
+    if (a2a) weight.assign(bytes.begin(), bytes.end());
+    fill_job(*fwd, l, true, epoch, 0, active, weight, paired);
+    fill_job(*bwd, l, false, epoch, 1, active, weight, paired);
     fwd->wait_start = bwd->wait_start = wait_start;
     if (a2a) {
         // every flow at once; the dom * dom flows into this domain share the
@@ -1288,15 +1364,17 @@ static int ag_jobs(const compass_problem *p, const Geometry &geo, const compass_
 static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_links *l, uint32_t epoch, int d,
                    uint64_t resident, bool gate_out, bool wait_start, Job jobs[4]) {
     // incoming fp32 partials carry twice the bytes of the outgoing bf16 sums
-    std::vector<int> active{0}, weight{2};
+    std::vector<int> active{0}, bytes{2};
     const bool dbl = two_rings(p);
-    if (dbl) { active.push_back(1); weight.push_back(2); }
+    if (dbl) { active.push_back(1); bytes.push_back(2); }
     if (p->send_dst) {
-        active.push_back(2); weight.push_back(1);
-        if (dbl) { active.push_back(3); weight.push_back(1); }
+        active.push_back(2); bytes.push_back(1);
+        if (dbl) { active.push_back(3); bytes.push_back(1); }
     }
+    std::vector<double> weight;
+    const bool paired = direction_weights(active, bytes, l, &weight);
     for (int r = 0; r < 4; ++r) {
-        fill_job(jobs[r], l, r % 2 == 0, epoch, r, active, weight);
+        fill_job(jobs[r], l, r % 2 == 0, epoch, r, active, weight, paired);
         jobs[r].wait_start = wait_start;
     }
     const size_t N = (size_t)p->N;
@@ -1384,7 +1462,7 @@ static void pool_jobs(Job *jobs, int count) {
         }
     }
     std::stable_sort(m.items.begin(), m.items.end(), [](const Item &a, const Item &b) { return a.seq < b.seq; });
-    m.engines = engines_for(first, std::vector<int>{first}, std::vector<int>{1}, 0);
+    m.engines = engines_for(first, std::vector<int>{first}, std::vector<double>{1.0}, 0);
     m.pool_depth = c.pool_depth;
     if (m.slice_default) m.slice = kPoolSlice;
 }
@@ -1769,10 +1847,13 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
 int op_sync() {
     int rc = ensure_init();
     if (rc != COMPASS_OK) return rc;
+    // a job ends within its own stall bound (the host timeout), then lets a
+    // failed job's copies land (the same bound again, at least 1 s); copy
+    // jobs still running past both are treated as copies in flight
     const double t0 = now_s();
     while (!pacers_idle()) {
-        if (now_s() - t0 > g_ctx.host_timeout + 1.0) {
-            g_ctx.async_err.store(COMPASS_ERR_TIMEOUT);
+        if (now_s() - t0 > 2.0 * g_ctx.host_timeout + 2.0) {
+            g_ctx.in_flight.store(true);
             break;
         }
         std::this_thread::yield();

@@ -359,3 +359,35 @@ def test_plain_gemm_refuses_degenerate_shapes():
     for it in (0, -1, 1 << 23):
         a, b = ctypes.c_double(), ctypes.c_double()
         assert lib.compass_probe_mfma(it, ctypes.byref(a), ctypes.byref(b)) == C.ERR_INVALID
+
+
+def test_binding_checks_shapes_element_sizes_and_contiguity():
+    # the binding rejects operands whose extents differ from what M, N, K and
+    # n imply before any library call (host tensors suffice: nothing runs)
+    torch = pytest.importorskip("torch")
+    M, N, K, n = 64, 32, 16, 4
+    i16 = lambda *s: torch.zeros(s, dtype=torch.int16)  # noqa: E731
+    f32 = lambda *s: torch.zeros(s, dtype=torch.float32)  # noqa: E731
+    sh = [i16(M // n, K) for _ in range(n)]
+    C.ag_problem(sh, i16(M, K), i16(N, K), i16(M, N), 0, "single")
+    with pytest.raises(ValueError, match=r"shards\[3\]"):
+        C.ag_problem(sh[:3] + [i16(M // n, K + 8)], i16(M, K), i16(N, K), i16(M, N), 0, "single")
+    with pytest.raises(ValueError, match="element size"):
+        C.ag_problem(sh, i16(M, K), i16(N, K), f32(M, N), 0, "single")
+    with pytest.raises(ValueError, match="contiguous"):
+        C.ag_problem(sh, i16(M, K), i16(K, N).t(), i16(M, N), 0, "single")
+    with pytest.raises(ValueError, match="split"):
+        C.ag_problem(sh[:3], i16(M, K), i16(N, K), i16(M, N), 0, "single")
+    parts = [f32(M // n, N) for _ in range(n)]
+    sends = [None] + [i16(M // n, N) for _ in range(n - 1)]
+    C.rs_problem(i16(M, K), i16(N, K), parts, f32(M, N), i16(M, N), sends, 0, "single")
+    with pytest.raises(ValueError, match=r"partial_src\[1\]"):
+        C.rs_problem(i16(M, K), i16(N, K), [parts[0], i16(M // n, N)] + parts[2:], f32(M, N), i16(M, N), sends, 0,
+                     "single")
+    with pytest.raises(ValueError, match="partial_stage"):
+        C.rs_problem(i16(M, K), i16(N, K), parts, i16(M, N), i16(M, N), sends, 0, "single")
+    with pytest.raises(ValueError, match=r"send_dst\[2\]"):
+        C.rs_problem(i16(M, K), i16(N, K), parts, f32(M, N), i16(M, N), sends[:2] + [i16(M // n, N - 8)] + sends[3:],
+                     0, "single")
+    with pytest.raises(ValueError, match="entries"):
+        C.rs_problem(i16(M, K), i16(N, K), parts, f32(M, N), i16(M, N), sends[:2], 0, "single")
