@@ -12,7 +12,9 @@ import os
 from typing import Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libcompass.so")
+# COMPASS_LIBRARY selects another build of the same library (the host
+# sanitizer build, libcompass_san.so, in CPU-only test runs)
+LIB_PATH = os.environ.get("COMPASS_LIBRARY") or os.path.join(_HERE, "libcompass.so")
 
 OK = 0
 ERR_INVALID = -1

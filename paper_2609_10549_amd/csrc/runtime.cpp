@@ -108,6 +108,11 @@ struct Item {
     int gate;   // host done flag to wait for before the item, -1: none
     double due_at = -1.0;   // paced, >= 0: due this long after the job started
     int seq = 0;            // position in the operator's transfer order (pooled jobs)
+    // pooled jobs: the link the item travels on (its direction's role), that
+    // link's rate (<= 0: unpaced) and the item's slice size
+    int link = 0;
+    double rate = 0.0;
+    size_t slice = 0;
 };
 
 struct Job {
@@ -460,21 +465,28 @@ constexpr double kCopyFixed = 10e-6;
 constexpr double kEngineBps = 38e9;
 
 // Engines per item for a paced job: the widest group (shortest item latency)
-// whose E / k groups still carry the link rate with `headroom` to spare; if
-// none does, one engine per item: the rate is then out of reach, and single
-// copies, E at a time, pay the fixed cost of a copy least often, so the link
-// comes closest to it (all E engines per small item would carry a fraction
-// of what single copies do). The first items of a job are
-// issued at once and land one group latency after the start, so too narrow
-// a group delays them all: at 268 GB/s with 22 MiB items, 10 % headroom left
-// groups of 2 engines (≈ 310 µs per item) where 5 % allows 4 (≈ 160 µs), and
-// the fused GPT-3 AllGather took 1429 against 1144 µs.
+// whose E / k groups still carry the link rate with `headroom` to spare. If
+// none does, the rate is out of reach, and the widest group that still moves
+// 90 % of what single copies do (E at a time, paying the fixed cost of a
+// copy least often): for small items that is one engine per item (all E
+// engines on a 1 MiB item would carry a fraction of what single copies do),
+// for large ones the whole set (a 22 MB item on one engine lands after
+// ~590 us, on four after ~155 us, for 5 % less throughput). The first items
+// of a job are issued at once and land one group latency after the start,
+// so too narrow a group delays them all: at 268 GB/s with 22 MiB items, 10 %
+// headroom left groups of 2 engines (≈ 310 µs per item) where 5 % allows 4
+// (≈ 160 µs), and the fused GPT-3 AllGather took 1429 against 1144 µs.
 static size_t group_width(double rate, size_t E, size_t item_bytes, double headroom) {
+    auto carried = [&](size_t k) {
+        const double lat = kCopyFixed + (double)item_bytes / ((double)k * kEngineBps);
+        return (double)(E / k) * (double)item_bytes / lat;
+    };
     for (size_t k = E; k >= 1; --k) {
         if (E % k) continue;
-        const double lat = kCopyFixed + (double)item_bytes / ((double)k * kEngineBps);
-        if ((double)(E / k) * (double)item_bytes / lat >= (1.0 + headroom) * rate) return k;
+        if (carried(k) >= (1.0 + headroom) * rate) return k;
     }
+    for (size_t k = E; k > 1; --k)
+        if (E % k == 0 && carried(k) >= 0.9 * carried(1)) return k;
     return 1;
 }
 
@@ -566,6 +578,7 @@ void Pacer::execute(Job &job) {
                     landed = hsa_signal_load_scacquire(issued[si]) <= 0;
                 if (landed) {
                     pd.landed = true;
+                    trace_event(role, job.epoch, "item_landed", pd.flag, 0);
                     if (paced && pd.model > 0) {
                         // latency correction, biased late: an early item only waits for its due time
                         const double ratio = (now - pd.issued_at) / pd.model;
@@ -607,6 +620,7 @@ void Pacer::execute(Job &job) {
                             o += len;
                         }
                         if (it.flag >= 0) pend.push_back({it.flag, first, issued.size() - first, due, now_s(), model, false});
+                        trace_event(role, job.epoch, "item_due_ns", it.flag, (size_t)std::max(0.0, (due - job_start) * 1e9));
                         if (!job.concurrent) link_free = due;
                         ++idx;
                         gate_ok = false;
@@ -659,17 +673,28 @@ void Pacer::execute(Job &job) {
     trace_event(role, job.epoch, "landed", -1, 0);
 }
 
-// Pooled (unpaced directions sharing every engine): the job holds the items
-// of every active ring direction in the operator's transfer order. Each
-// engine keeps at most `pool_depth` copies queued; whenever one has room it
-// takes the next slice of the first item, in that order, that is ready (its
-// gate open) and has bytes left. An outgoing sum follows the incoming
-// partial of its partition in the order, so a finished chunk's send goes out
-// ahead of later arrivals, and no engine idles while either direction has
-// ready work (split per direction, the incoming fp32 partials and the gated
-// outgoing sums leave engines of one side idle while the other is behind).
-// Items are cut into equal slices of at most `slice` bytes; an item's flag is
-// published when all of its slices have landed.
+// Pooled (the directions of one operator sharing every engine): the job
+// holds the items of every active ring direction in the operator's transfer
+// order. Each engine keeps at most `pool_depth` copies queued; whenever one
+// has room it takes the next slice of the ready item (gate open) with bytes
+// left whose due time is earliest, the first in transfer order among equal
+// ones. An item's flag is published when all of its slices have landed and
+// its due time has passed.
+//
+// Due times: an unpaced item (rate <= 0) is due at once, so the engines
+// serve the items in transfer order: an outgoing sum follows the incoming
+// partial of its partition, a finished chunk's send goes out ahead of later
+// arrivals, and no engine idles while either direction has ready work. A
+// paced item is due when its link would have delivered it: its link carries
+// one item at a time at the link's rate, so item i is due at
+// max(due of the link's previous item, when its gate opened) + bytes / rate
+// (an item with a due time of its own, a ring whose hops differ, keeps it).
+// The copy engines move a paced item as early as their queues allow and the
+// flag waits for the due time: the kernel sees exactly the link's arrival
+// times, and no item lands late for lack of engines while another
+// direction's engines idle (engines split per direction, the first items of
+// the faster direction of a 4 : 1 ring landed 130 us after their due times).
+// Items are cut into equal slices of at most their `slice` bytes.
 void Pacer::execute_pooled(Job &job) {
     Ctx &c = *ctx;
     trace_event(role, job.epoch, "job_begin", -1, 0);
@@ -677,27 +702,61 @@ void Pacer::execute_pooled(Job &job) {
         c.async_err.store(COMPASS_ERR_TIMEOUT);
         return;
     }
+    const double job_start = now_s();
     trace_event(role, job.epoch, "start_seen", -1, 0);
     const size_t E = job.engines.size();
     const int depth = std::max(1, job.pool_depth);
+    constexpr double kUnknown = -1.0;
     struct State {
         size_t off = 0, per = 0;
         int inflight = 0;
         bool ready = false, done = false;
+        double opened = 0.0;      // when the gate opened (the job start if none)
+        double due = kUnknown;    // earliest publication
     };
     struct Copy {
         hsa_signal_t sg;
-        size_t item, eng;
+        size_t item, eng, len;
     };
     std::vector<State> st(job.items.size());
     size_t remaining = 0;
+    int links = 1;
     for (size_t i = 0; i < job.items.size(); ++i) {
         const Item &it = job.items[i];
-        const size_t k = std::max<size_t>(1, (it.bytes + job.slice - 1) / job.slice);
+        const size_t slice = it.slice ? it.slice : job.slice;
+        const size_t k = std::max<size_t>(1, (it.bytes + slice - 1) / slice);
         st[i].per = std::max<size_t>(256, ((it.bytes + k - 1) / k + 255) & ~(size_t)255);
         st[i].ready = it.gate < 0;
+        st[i].opened = job_start;
+        links = std::max(links, it.link + 1);
         ++remaining;
     }
+    // per link: when it has delivered its last item with a due time, and
+    // the next item (in order) still without one
+    std::vector<double> link_free(links, job_start);
+    std::vector<size_t> next_due(links, 0);
+    auto assign_dues = [&]() {
+        for (int L = 0; L < links; ++L) {
+            size_t &i = next_due[L];
+            for (; i < job.items.size(); ++i) {
+                const Item &it = job.items[i];
+                if (it.link != L) continue;
+                State &s = st[i];
+                if (!s.ready) break;   // later items of this link wait for it
+                if (it.due_at >= 0) {
+                    s.due = job_start + it.due_at;
+                } else if (it.rate > 0) {
+                    s.due = std::max(link_free[L], s.opened) + (double)it.bytes / it.rate;
+                    link_free[L] = s.due;
+                } else {
+                    s.due = 0.0;
+                }
+                if (it.flag >= 0 && s.due > 0) trace_event(role, job.epoch, "item_due_ns", it.flag,
+                                                          (size_t)((s.due - job_start) * 1e9));
+            }
+        }
+    };
+    assign_dues();
     std::vector<Copy> fly;
     std::vector<int> load(E, 0);
     size_t rr = 0, first_open = 0;
@@ -710,22 +769,27 @@ void Pacer::execute_pooled(Job &job) {
                 continue;
             }
             --load[fly[i].eng];
+            trace_event(role, job.epoch, "copy_done", __builtin_ctz(job.engines[fly[i].eng]), fly[i].len);
             State &s = st[fly[i].item];
             --s.inflight;
             fly[i] = fly.back();
             fly.pop_back();
             progress = true;
         }
+        const double now = now_s();
+        bool opened = false;
         for (size_t i = first_open; i < job.items.size(); ++i) {
             const Item &it = job.items[i];
             State &s = st[i];
             if (s.done) continue;
             if (!s.ready && (int32_t)(__atomic_load_n(&c.hw[kHwDone + it.gate], __ATOMIC_ACQUIRE) - job.epoch) >= 0) {
                 s.ready = true;
+                s.opened = now;
+                opened = true;
                 progress = true;
                 trace_event(role, job.epoch, "gate_open", it.gate, 0);
             }
-            if (s.ready && s.inflight == 0 && s.off >= it.bytes) {
+            if (s.ready && s.inflight == 0 && s.off >= it.bytes && s.due != kUnknown && now >= s.due) {
                 if (it.flag >= 0) {
                     __atomic_store_n(&c.hw[kHwFlags + it.flag], job.epoch, __ATOMIC_RELEASE);
                     trace_event(role, job.epoch, "flag", it.flag, 0);
@@ -735,6 +799,7 @@ void Pacer::execute_pooled(Job &job) {
                 progress = true;
             }
         }
+        if (opened) assign_dues();
         while (first_open < job.items.size() && st[first_open].done) ++first_open;
         for (;;) {
             size_t e = E;
@@ -744,11 +809,11 @@ void Pacer::execute_pooled(Job &job) {
             }
             if (e == E) break;
             size_t pick = job.items.size();
-            for (size_t i = first_open; i < job.items.size(); ++i)
-                if (st[i].ready && st[i].off < job.items[i].bytes) {
-                    pick = i;
-                    break;
-                }
+            for (size_t i = first_open; i < job.items.size(); ++i) {
+                const State &s = st[i];
+                if (!s.ready || s.due == kUnknown || s.off >= job.items[i].bytes) continue;
+                if (pick == job.items.size() || s.due < st[pick].due) pick = i;
+            }
             if (pick == job.items.size()) break;
             const Item &it = job.items[pick];
             State &s = st[pick];
@@ -764,7 +829,7 @@ void Pacer::execute_pooled(Job &job) {
                 return;
             }
             trace_event(role, job.epoch, "slice", __builtin_ctz(job.engines[e]), len);
-            fly.push_back({sg, pick, e});
+            fly.push_back({sg, pick, e, len});
             ++load[e];
             ++s.inflight;
             s.off += len;
@@ -774,7 +839,11 @@ void Pacer::execute_pooled(Job &job) {
         if (progress) {
             last_progress = now_s();
         } else {
-            if (now_s() - last_progress > c.host_timeout) {
+            // waiting for a due time is not a stall
+            double horizon = last_progress;
+            for (size_t i = first_open; i < job.items.size(); ++i)
+                if (!st[i].done && st[i].due != kUnknown) horizon = std::max(horizon, st[i].due);
+            if (now_s() - horizon > c.host_timeout) {
                 c.async_err.store(COMPASS_ERR_TIMEOUT);
                 return;
             }
@@ -1198,22 +1267,30 @@ static void touch_all(GemmParams &g, int nparts) {
     }
 }
 
-// Row tiles ordered by the schedule position of the last partition they
-// touch; touched partitions from the identity row map.
-static void order_by_schedule(GemmParams &g, int cfg, const Geometry &geo, int M, bool main_gate) {
+// Row tiles ordered by when the last partition they touch is expected to
+// land (ties: its schedule position); touched partitions from the identity
+// row map. `arrive[q]` is that expectation for partition q (the schedule
+// position itself when the links give no better one).
+static void order_by_arrival(GemmParams &g, int cfg, const Geometry &geo, int M, bool main_gate,
+                             const double *arrive) {
     const int bm = tile_rows(cfg);
-    std::vector<std::pair<int, int>> key;
+    struct Key { double t; int pos, tile; };
+    std::vector<Key> key;
     for (int t = 0; t < g.tiles_m; ++t) {
         const int r0 = t * bm, r1 = std::min(M, r0 + bm) - 1;
         const int p0 = part_of_row(geo, r0), p1 = part_of_row(geo, r1);
-        int k = 0;
-        for (int q = p0; q <= p1; ++q) k = std::max(k, geo.pos[q]);
+        Key k{0.0, 0, t};
+        for (int q = p0; q <= p1; ++q) {
+            k.t = std::max(k.t, arrive[q]);
+            k.pos = std::max(k.pos, geo.pos[q]);
+        }
         g.rt_lo[t] = (uint8_t)p0;
         g.rt_hi[t] = (uint8_t)p1;
-        key.push_back({k, t});
+        key.push_back(k);
     }
-    std::stable_sort(key.begin(), key.end());
-    for (int i = 0; i < g.tiles_m; ++i) g.rt_order[i] = (uint16_t)key[i].second;
+    std::stable_sort(key.begin(), key.end(),
+                     [](const Key &a, const Key &b) { return a.t < b.t || (a.t == b.t && a.pos < b.pos); });
+    for (int i = 0; i < g.tiles_m; ++i) g.rt_order[i] = (uint16_t)key[i].tile;
     // AllGather: the tiles of one arriving partition are consecutive in the
     // ready order and cannot start before it lands. Short super-blocks deal
     // them out over all XCD queues, and the second workgroup of each CU
@@ -1300,6 +1377,46 @@ static int hop_arrivals(const compass_problem *p, const compass_links *l, int d,
     out->resize((size_t)d * (p->n - 1));
     const int k = ring_arrivals(p->n, p->rank, piece_bytes, l->hop_Bps, d, out->data(), (int)out->size());
     return k < 0 ? k : COMPASS_OK;
+}
+
+// Expected arrival of every partition of a fused operator (seconds after
+// its start; resident partitions at 0), used only to order the tiles. Each
+// ring direction delivers its partitions one after another in schedule
+// order, a partition taking its bytes over the direction's rate; unpaced or
+// half-paced links count as equal rates, so that the order falls back to
+// the schedule's. Per-hop rates take the store-and-forward arrival times;
+// the AlltoAll pattern keeps the schedule order.
+static int expected_arrivals(const compass_problem *p, const Geometry &geo, const compass_links *l, uint64_t resident,
+                             double *t) {
+    for (int q = 0; q < geo.P; ++q) t[q] = (double)geo.pos[q];
+    if (p->ring == COMPASS_RING_ALLTOALL) return COMPASS_OK;
+    const double row_bytes = p->pattern == COMPASS_AG_GEMM ? 2.0 * p->K : 4.0 * p->N;
+    if (l->hop_Bps) {
+        std::vector<double> due;
+        const int rc = hop_arrivals(p, l, 1, (double)geo.rows * row_bytes, &due);
+        if (rc != COMPASS_OK) return rc;
+        for (int s = 0; s < geo.P; ++s) {
+            const int q = geo.sched[s];
+            t[q] = (resident >> q) & 1ull ? 0.0 : due[(size_t)std::min(std::max(s, 1), geo.P - 1) - 1];
+        }
+        return COMPASS_OK;
+    }
+    const bool rated = l->fwd_Bps > 0 && (!geo.dbl || l->bwd_Bps > 0);
+    double clock[2] = {0.0, 0.0};
+    for (int s = 0; s < geo.P; ++s) {
+        const int q = geo.sched[s];
+        if ((resident >> q) & 1ull) {
+            t[q] = 0.0;
+            continue;
+        }
+        int off, cnt;
+        part_rows(geo, geo.rows, q, &off, &cnt);
+        const bool fwd = part_fwd(geo, q);
+        const double rate = rated ? (fwd ? l->fwd_Bps : l->bwd_Bps) : 1.0;
+        clock[fwd ? 0 : 1] += (double)cnt * row_bytes / rate;
+        t[q] = clock[fwd ? 0 : 1];
+    }
+    return COMPASS_OK;
 }
 
 // ---------------------------------------------------------------- AllGather jobs
@@ -1427,11 +1544,14 @@ static int rs_jobs(const compass_problem *p, const Geometry &geo, const compass_
     return COMPASS_OK;
 }
 
-// Unpaced operators with more than one active direction let the directions
-// share every copy engine (COMPASS_OPT_POOL > 0): their items merge, in the
-// operator's transfer order, into the first such job, which runs pooled on
-// its role's thread; the other jobs are left empty. Paced links, per-hop due
-// times and the AlltoAll pattern keep a job per direction, and so do copies
+// The directions of an operator share every copy engine when all of its
+// copies stay in device memory (COMPASS_OPT_POOL > 0): their items merge, in
+// the operator's transfer order, into the first such job, which runs pooled
+// on its role's thread (earliest due slice first); the other jobs are left
+// empty. This covers paced links (with one direction too: its items then no
+// longer wait for engine groups), per-hop due times and unpaced operators
+// with more than one active direction. The AlltoAll pattern (flows sharing
+// a link, each paced on its own) keeps a job per direction, and so do copies
 // to or from host memory: across PCIe the link, not the engines, is the
 // limit, a copy takes milliseconds, and a pooled engine's queue would hold
 // an outgoing sum behind incoming partials that a direction of its own
@@ -1441,17 +1561,25 @@ static void pool_jobs(Job *jobs, int count) {
     Ctx &c = g_ctx;
     if (c.pool_depth <= 0) return;
     int first = -1, active = 0;
+    bool paced = false;
     for (int r = 0; r < count; ++r) {
         if (jobs[r].items.empty()) continue;
-        if (jobs[r].rate > 0 || jobs[r].concurrent) return;
+        if (jobs[r].concurrent) return;
         for (const Item &it : jobs[r].items)
-            if (it.due_at >= 0 || it.src_agent.handle != c.gpu.handle || it.dst_agent.handle != c.gpu.handle) return;
+            if (it.src_agent.handle != c.gpu.handle || it.dst_agent.handle != c.gpu.handle) return;
+        paced |= jobs[r].rate > 0;
+        for (const Item &it : jobs[r].items) paced |= it.due_at >= 0;
         if (first < 0) first = r;
         ++active;
     }
-    if (active < 2) return;
+    if (active < 1 || (!paced && active < 2)) return;
     Job &m = jobs[first];
     for (int r = 0; r < count; ++r) {
+        for (Item &it : jobs[r].items) {
+            it.link = r;
+            it.rate = jobs[r].rate;
+            it.slice = !jobs[r].slice_default ? jobs[r].slice : paced ? kDefaultSlice : kPoolSlice;
+        }
         if (r == first) continue;
         for (Item &it : jobs[r].items) m.items.push_back(it);
         jobs[r].items.clear();
@@ -1464,7 +1592,6 @@ static void pool_jobs(Job *jobs, int count) {
     std::stable_sort(m.items.begin(), m.items.end(), [](const Item &a, const Item &b) { return a.seq < b.seq; });
     m.engines = engines_for(first, std::vector<int>{first}, std::vector<double>{1.0}, 0);
     m.pool_depth = c.pool_depth;
-    if (m.slice_default) m.slice = kPoolSlice;
 }
 
 // Partitions in place before the operator starts: the rank's own chunk
@@ -1645,7 +1772,9 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 && geo.sub == 1 ? geo.rows : min_part_rows(geo),
                               lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
-    order_by_schedule(g, cfg, geo, p->M, true);
+    double arrive[2 * kMaxRanks];
+    if ((rc = expected_arrivals(p, geo, l, resident_mask(p, geo), arrive)) != COMPASS_OK) return rc;
+    order_by_arrival(g, cfg, geo, p->M, true, arrive);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
@@ -1670,7 +1799,9 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     init_params(g, epoch);
     const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l), true);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
-    order_by_schedule(g, cfg, geo, p->M, false);
+    double arrive[2 * kMaxRanks];
+    if ((rc = expected_arrivals(p, geo, l, res, arrive)) != COMPASS_OK) return rc;
+    order_by_arrival(g, cfg, geo, p->M, false, arrive);
     g.gate = kGateEpilogue;
     g.nparts = geo.P;
     g.resident_mask = res;
