@@ -272,6 +272,26 @@ int compass_gemm(int M, int N, int K, const void *A, const void *W, void *C,
 int compass_transfer(const compass_problem *p, const compass_links *links, void *stream);
 int compass_sequential(const compass_problem *p, const compass_links *links, void *stream);
 
+/* ---- compass_gemm for callers that cannot allocate ------------------------
+ * For code under HIP graph capture, tight serving loops and harnesses that
+ * forbid allocation: the plain GEMM of compass_gemm (same arguments, layout,
+ * limits and result: C = A W^T (+ P), fp32 accumulation, one bf16 rounding)
+ * without any allocation, library initialisation or copy-side state. Its
+ * only scratch, the persistent scheduler's ticket queues and exit counter
+ * (256 bytes), lives in a device array of the library's code object, held
+ * by each GPU until the process ends; the first call on a device resolves
+ * its address. The launch never splits K, so shapes with few output tiles
+ * run slower than compass_gemm (which splits K into a workspace). The call
+ * enqueues a scratch-clearing kernel and the GEMM on `stream`. Calls that
+ * overlap on one GPU (concurrent streams) race on the shared scratch; issue
+ * them on one stream. Errors: COMPASS_ERR_INVALID for a bad shape or NULL
+ * operand, COMPASS_ERR_UNSUPPORTED beyond the size limits (M above the
+ * 65536 rows of the tile table, A or W above 1 GiB, M x N fp32 above 2 GiB)
+ * or on a device other than gfx950, COMPASS_ERR_HIP when a launch fails;
+ * all before anything is enqueued except the last. */
+int compass_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C,
+                         const float *P, void *stream);
+
 /* Wait until the copy side of every enqueued operator has finished and the
  * device is idle; return the pending asynchronous status (COMPASS_OK or
  * COMPASS_ERR_TIMEOUT) and clear it. COMPASS_ERR_IN_FLIGHT (not cleared) when

@@ -28,7 +28,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libcompass.so")
 SAN_LIB = os.path.join(HERE, "libcompass_san.so")
-SOURCES = ["kernels.hip", "runtime.cpp", "model.cpp", "abi.cpp"]
+SOURCES = ["kernels.hip", "noalloc.hip", "runtime.cpp", "model.cpp", "abi.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -112,6 +112,8 @@ _SIGS = {
                                            ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_gemm": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "compass_gemm_noalloc": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "compass_transfer": (ctypes.c_int, [ctypes.POINTER(compass_problem), ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_sequential": (ctypes.c_int, [ctypes.POINTER(compass_problem), ctypes.POINTER(compass_links), ctypes.c_void_p]),
     "compass_sync": (ctypes.c_int, []),
@@ -310,6 +312,17 @@ def compass_gemm(A, W, C, P=None, stream=None) -> None:
     _need(C, "C", (M, N), 2)
     _need(P, "P", (M, N), 4)
     _check(lib().compass_gemm(M, N, K, _addr(A), _addr(W), _addr(C), _addr(P), _stream(stream)), "compass_gemm")
+
+
+def compass_gemm_noalloc(A, W, C, P=None, stream=None) -> None:
+    M, K = A.shape
+    N = W.shape[0]
+    _need(A, "A", (M, K), 2)
+    _need(W, "W", (N, K), 2)
+    _need(C, "C", (M, N), 2)
+    _need(P, "P", (M, N), 4)
+    _check(lib().compass_gemm_noalloc(M, N, K, _addr(A), _addr(W), _addr(C), _addr(P), _stream(stream)),
+           "compass_gemm_noalloc")
 
 
 def compass_transfer(problem: Problem, lk: compass_links | None = None, stream=None) -> None:

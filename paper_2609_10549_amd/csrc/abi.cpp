@@ -26,6 +26,10 @@ int compass_gemm(int M, int N, int K, const void *A, const void *W, void *C, con
     return op_gemm(M, N, K, A, W, C, P, stream);
 }
 
+int compass_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream) {
+    return op_gemm_noalloc(M, N, K, A, W, C, P, stream);
+}
+
 int compass_transfer(const compass_problem *p, const compass_links *links, void *stream) {
     return op_transfer(p, links, stream);
 }

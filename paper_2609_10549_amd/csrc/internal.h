@@ -24,6 +24,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream);
 int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream);
 int op_decomp(const compass_problem *p, int d, const compass_links *l, void *stream);
 int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream);
+int op_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C, const float *P, void *stream);
 int op_transfer(const compass_problem *p, const compass_links *l, void *stream);
 int op_partition_layout(int pattern, int ring, int n, int rank, int M, const compass_links *l, int32_t *order,
                         int32_t *row0, int32_t *rows, int cap);
