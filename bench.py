@@ -55,6 +55,10 @@ def parse():
     ap.add_argument("--no-mlp", action="store_true", help="skip the fc1 / fc2 MLP pair under ops")
     ap.add_argument("--profile-only", action="store_true",
                     help="run only the timed steps (for rocprofv3); print the JSON line")
+    ap.add_argument("--rates", default=None,
+                    help="slow-ring rates of the AllGather and the ReduceScatter in GB/s, comma-separated "
+                         "(the fast ring runs 4x): skips the rate search, so that a profiled run uses the "
+                         "rates an unprofiled one found")
     return ap.parse_args()
 
 
@@ -100,10 +104,11 @@ def main():
     t_gemm_rs = CAL.time_call(lambda: C.compass_gemm(rs.A, rs.W, rs.C, rs.stage), reps=7, warmup=3)
     per_link_ag = CAL.ring_bytes_per_link("ag", ag.M, ag.N, ag.K, n, "double")
     per_link_rs = CAL.ring_bytes_per_link("rs", rs.M, rs.N, rs.K, n, "double")
+    fixed = [float(x) * 1e9 for x in args.rates.split(",")] if args.rates else [None, None]
     lk_ag, tx_ag, hist_ag = balanced_rates(C, CAL, per_link_ag, t_gemm_ag,
-                                           lambda lk: C.compass_transfer(ag.problem, lk))
+                                           lambda lk: C.compass_transfer(ag.problem, lk), fixed[0])
     lk_rs, tx_rs, hist_rs = balanced_rates(C, CAL, per_link_rs, t_gemm_rs,
-                                           lambda lk: C.compass_transfer(rs.problem, lk))
+                                           lambda lk: C.compass_transfer(rs.problem, lk), fixed[1])
 
     # ---------------------------------------------------------------- strategy (Algorithm 1)
     cal = CAL.load()
@@ -265,15 +270,16 @@ class RSBuffers:
         self.problem = C.rs_problem(self.A, self.W, self.partials, self.stage, self.C, self.sends, rank, ring)
 
 
-def balanced_rates(C, CAL, per_link, t_gemm, transfer):
+def balanced_rates(C, CAL, per_link, t_gemm, transfer, fixed=None):
     """4 : 1 ring rates for the double ring in halves: the slow direction at
     the rate that makes its transfer (per_link bytes) as long as the GEMM
     alone, the fast one at four times that; lowered to what the copy engines
-    deliver while a paced transfer takes more than 5 % over its link time.
-    Returns (links, transfer-alone time, [(slow rate, measured time), ...])."""
-    bwd = per_link / (t_gemm / LAMBDA_TARGET)
+    deliver while a paced transfer takes more than 5 % over its link time
+    (`fixed`: that slow rate, no search). Returns (links, transfer-alone
+    time, [(slow rate, measured time), ...])."""
+    bwd = fixed if fixed else per_link / (t_gemm / LAMBDA_TARGET)
     hist = []
-    for _ in range(4):
+    for _ in range(1 if fixed else 4):
         lk = C.links(RATE_RATIO * bwd, bwd)
         tx = CAL.time_call(lambda: transfer(lk), reps=3)
         hist.append((bwd, tx))

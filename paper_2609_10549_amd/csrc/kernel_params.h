@@ -60,12 +60,15 @@ struct GemmParams {
     int spread_wait;
     uint32_t launch_seq;
     uint32_t *cu_slots;
-    // split K: tile position t, slice j = work position t * ksplit + j, K
-    // range [j kslice, (j + 1) kslice). Every slice stores its fp32 partial
-    // tile at split_ws[(t * ksplit + j) * BM * BN]; the slice that counts
-    // split_cnt[t] up to ksplit sums the partials in slice order and runs the
-    // epilogue. ksplit == 1: no split (kslice = K).
-    int ksplit, kslice;
+    // split K: work positions below split_from are whole tiles (tile
+    // position = work position); from split_from on, tile position
+    // t = split_from + u, slice j = work position split_from + u * ksplit + j,
+    // K range [j kslice, (j + 1) kslice). Every slice stores its fp32 partial
+    // tile at split_ws[(u * ksplit + j) * BM * BN]; the slice that counts
+    // split_cnt[u] up to ksplit sums the partials in slice order and runs the
+    // epilogue. ksplit == 1: no split (kslice = K); split_from == 0: every
+    // tile split.
+    int ksplit, kslice, split_from;
     uint32_t *split_cnt;
     float *split_ws;
     // gating: flag index of partition p is flag_base + p. Arrival flags live

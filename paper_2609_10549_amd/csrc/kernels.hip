@@ -301,7 +301,7 @@ void gemm_kernel(const GemmParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave >> 1) * WM;
     const int wn0 = (wave & 1) * WN;
-    const int total = p.tiles_m * p.tiles_n * p.ksplit;
+    const int total = p.split_from + (p.tiles_m * p.tiles_n - p.split_from) * p.ksplit;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
     const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
@@ -336,11 +336,14 @@ void gemm_kernel(const GemmParams p) {
     int pos = s_pos;
 
     while (pos < total) {
-        // work position -> (tile position, K slice)
-        const int tpos = p.ksplit > 1 ? pos / p.ksplit : pos;
-        const int slice = pos - tpos * p.ksplit;
-        const int kb = slice * p.kslice;
-        const int ke = min(p.K, kb + p.kslice);
+        // work position -> (tile position, K slice); `split`: this tile's K
+        // is split, its u-th split tile (u = tile position - split_from)
+        const bool split = p.ksplit > 1 && pos >= p.split_from;
+        const int u = split ? (pos - p.split_from) / p.ksplit : 0;
+        const int tpos = split ? p.split_from + u : pos;
+        const int slice = split ? pos - p.split_from - u * p.ksplit : 0;
+        const int kb = split ? slice * p.kslice : 0;
+        const int ke = split ? min(p.K, kb + p.kslice) : p.K;
         // tile position -> (row-tile ordinal, column tile): group_m rows at a time
         const int gsz = p.group_m * p.tiles_n;
         const int grp = tpos / gsz;
@@ -480,8 +483,8 @@ void gemm_kernel(const GemmParams p) {
         // the slice that completes the tile's count sums all of them in
         // slice order, so the result does not depend on which one was last
         bool finish = true;
-        if (p.ksplit > 1) {
-            float *ws = p.split_ws + (size_t)(tpos * p.ksplit + slice) * (BM * BN);
+        if (split) {
+            float *ws = p.split_ws + (size_t)(u * p.ksplit + slice) * (BM * BN);
             through_patch([&](int row, int col, f32x4 x) {
                 *reinterpret_cast<f32x4 *>(ws + row * BN + col) = x;
             });
@@ -492,10 +495,10 @@ void gemm_kernel(const GemmParams p) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
-                const uint32_t old = __hip_atomic_fetch_add(&p.split_cnt[tpos], 1u, __ATOMIC_RELAXED,
+                const uint32_t old = __hip_atomic_fetch_add(&p.split_cnt[u], 1u, __ATOMIC_RELAXED,
                                                             __HIP_MEMORY_SCOPE_AGENT);
                 const bool last = old + 1u == (uint32_t)p.ksplit;
-                if (last) __hip_atomic_store(&p.split_cnt[tpos], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (last) __hip_atomic_store(&p.split_cnt[u], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 s_last = last;
             }
             __syncthreads();   // the partial loads below are issued after the count
@@ -514,8 +517,8 @@ void gemm_kernel(const GemmParams p) {
         if (RS && traced && tid == 0) t_gate = rtc32();
 
         if (finish) {
-            if (p.ksplit > 1) {
-                const float *ws0 = p.split_ws + (size_t)tpos * p.ksplit * (BM * BN);
+            if (split) {
+                const float *ws0 = p.split_ws + (size_t)u * p.ksplit * (BM * BN);
                 // B elements of 4 per thread at a time, all their slices' loads
                 // (and the partial sum's) in flight at once, then each summed in
                 // slice order: the workspace is uncached, so every load costs a

@@ -87,6 +87,9 @@ constexpr int kSchedFineQueues = 1, kSchedSpread = 2, kSchedSplitK = 4;
 // split-K workspace: one fp32 partial tile per workgroup slot (the largest
 // of 256 x 256 on one workgroup per CU and 128 x 128 on two)
 constexpr int kMinSliceK = 512;      // K depth of a slice at least
+constexpr int kSplitWsTiles = 2;     // workspace: this many 256 x 256 fp32 partial tiles per CU
+constexpr int kTailMinK = 8192;      // fused AllGather: split the tail's K from this depth on
+constexpr int kTailSliceK = 2048;    // ... into slices at least this deep, at most 4
 // host_words layout (pinned, coherent host memory): start word, error word,
 // done flags (kernel -> copy side), arrival flags (copy side -> kernel)
 constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
@@ -295,7 +298,7 @@ static int ensure_init() {
         // Uncached, so that partial tiles written on one XCD are read on
         // another without cache maintenance. Held until the process ends
         // (uncached memory is never freed once a kernel has read it).
-        const size_t ws = (size_t)c.num_cu * std::max(256 * 256, 2 * 128 * 128) * sizeof(float);
+        const size_t ws = (size_t)kSplitWsTiles * c.num_cu * std::max(256 * 256, 2 * 128 * 128) * sizeof(float);
         if ((e = hipExtMallocWithFlags((void **)&c.split_ws, ws, hipDeviceMallocUncached)) != hipSuccess)
             return hip_fail(e, "split-K workspace");
         c.split_ws_bytes = ws;
@@ -1158,10 +1161,11 @@ static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.
     if (g_ctx.tile_override == 2) return kTile128;
     // A plain GEMM takes the larger (faster) tile when it still fills every
     // CU. The fused AllGather needs several tiles per arriving partition; it
-    // takes it only when a partition spans whole 256-row tiles and the GEMM
-    // is at least four waves of 256 x 256 tiles, or two waves with
-    // computation clearly dominating the transfer (estimated lambda >= 2),
-    // where the larger tile's speed matters more than arrival granularity.
+    // takes it when a partition spans whole 256-row tiles and the GEMM is at
+    // least two waves of 256 x 256 tiles (the tiles of the last arrivals then
+    // split K, see set_tail_split): on the GPT-3 AllGather (3 waves, 4 : 1
+    // double ring, lambda ~ 1) 1156 us against 1361 us with 128 x 128 tiles,
+    // whose main loop runs ~15 % slower per flop.
     // The fused ReduceScatter takes 256 x 256 only when computation dominates
     // (estimated lambda >= 1) over at least two waves: with one workgroup per
     // CU its chunks finish in bursts of a whole wave and the sends of the last
@@ -1172,7 +1176,7 @@ static int pick_tile(int M, int N, bool gated, int prow = 0, double lam_est = 0.
         const bool whole = prow >= 256 && prow % 256 == 0;
         const long cu = g_ctx.num_cu;
         if (rs) return whole && t256 >= 2 * cu && lam_est >= 1.0 ? kTile256 : kTile128;
-        return whole && (t256 >= 4 * cu || (t256 >= 2 * cu && lam_est >= 2.0)) ? kTile256 : kTile128;
+        return whole && t256 >= 2 * cu ? kTile256 : kTile128;
     }
     return t256 >= g_ctx.num_cu ? kTile256 : kTile128;
 }
@@ -1258,6 +1262,32 @@ static void set_split(GemmParams &g, int cfg) {
     g.grid = std::min(tiles * sp, slots);
     g.nq = g.grid >= kMaxQueues ? kMaxQueues : 1;
     g.q_size = std::max(1, g.grid / g.nq);
+}
+
+// Tail split of a fused AllGather with 256 x 256 tiles: a tile runs K / 64
+// pipeline stages (~300 us at K = 12288), so the tiles of the partitions
+// that land last would keep a few dozen CUs busy long after the last arrival
+// while the others idle (GPT-3 AllGather, 4 : 1 ring: 250 us of tail on at
+// most 96 of 256 CUs). The row tiles of the ready order's last two groups
+// (one partition each) split K into s slices, s = the workgroup slots over a
+// group's tiles, at most 4, each at least kTailSliceK deep; the rest of the
+// launch runs whole tiles. Only for K >= kTailMinK, where a whole tile's
+// latency dwarfs the partial tiles' round trip through the workspace.
+static void set_tail_split(GemmParams &g, int cfg) {
+    Ctx &c = g_ctx;
+    if (!(c.sched & kSchedSplitK) || !c.split_ws || g.ksplit > 1 || g.K < kTailMinK) return;
+    const int groups = (g.tiles_m + g.group_m - 1) / g.group_m;
+    if (groups < 4 || g.tiles_m % g.group_m) return;
+    const int tail_groups = 2;
+    const int tail_tiles = tail_groups * g.group_m * g.tiles_n;
+    const int slots = g.grid;
+    int sp = std::min(4, std::min(slots / (g.group_m * g.tiles_n), g.K / kTailSliceK));
+    const size_t tile_bytes = (size_t)tile_rows(cfg) * tile_cols(cfg) * sizeof(float);
+    while (sp > 1 && (size_t)tail_tiles * sp * tile_bytes > c.split_ws_bytes) --sp;
+    if (sp < 2 || tail_tiles > kMaxSplitTiles) return;
+    g.ksplit = sp;
+    g.kslice = ((g.K + sp - 1) / sp + 63) / 64 * 64;
+    g.split_from = (groups - tail_groups) * g.group_m * g.tiles_n;
 }
 
 static void touch_all(GemmParams &g, int nparts) {
@@ -1654,8 +1684,8 @@ static int launch(const GemmParams &g0, int cfg, bool rs, hipStream_t s) {
         g.tile_trace = c.tile_trace;
         g.trace_base = c.trace_used;
         g.trace_cap = c.trace_cap;
-        c.trace_used = std::min<uint64_t>(c.trace_cap,
-                                          (uint64_t)c.trace_used + (uint64_t)g0.tiles_m * g0.tiles_n * g0.ksplit);
+        const uint64_t work = (uint64_t)g0.split_from + ((uint64_t)g0.tiles_m * g0.tiles_n - g0.split_from) * g0.ksplit;
+        c.trace_used = std::min<uint64_t>(c.trace_cap, (uint64_t)c.trace_used + work);
     }
     const bool timed = c.timing && c.timed_count < Ctx::kTimed;
     if (timed) (void)hipEventRecord(c.ev_begin[c.timed_count], s);
@@ -1772,9 +1802,14 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 && geo.sub == 1 ? geo.rows : min_part_rows(geo),
                               lambda_estimate(p, geo, l));
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
+    // 256-row tiles: one row-tile group per partition, so that the dealing
+    // and the tail split follow partitions
+    if (cfg == kTile256 && geo.sub == 1 && geo.fb == 0.5 && min_part_rows(geo) % 256 == 0)
+        g.group_m = std::max(1, std::min(4, min_part_rows(geo) / 256));
     double arrive[2 * kMaxRanks];
     if ((rc = expected_arrivals(p, geo, l, resident_mask(p, geo), arrive)) != COMPASS_OK) return rc;
     order_by_arrival(g, cfg, geo, p->M, true, arrive);
+    if (cfg == kTile256) set_tail_split(g, cfg);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
@@ -1799,8 +1834,15 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     init_params(g, epoch);
     const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l), true);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
+    // ReduceScatter tiles compute before their partial is needed, so they
+    // run in ring-step order (a step's partitions on both rings together),
+    // not in arrival order: under a 4 : 1 ring the faster ring's partials
+    // land early, and taking their tiles first left the slower ring's last
+    // partitions computing long after their partials landed, their sends
+    // then queued one after another on the slow link (GPT-3 ReduceScatter:
+    // 220 us after the kernel)
     double arrive[2 * kMaxRanks];
-    if ((rc = expected_arrivals(p, geo, l, res, arrive)) != COMPASS_OK) return rc;
+    for (int q = 0; q < geo.P; ++q) arrive[q] = (double)geo.pos[q];
     order_by_arrival(g, cfg, geo, p->M, false, arrive);
     g.gate = kGateEpilogue;
     g.nparts = geo.P;

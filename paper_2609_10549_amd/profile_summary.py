@@ -5,6 +5,8 @@
         <copy_write_dir> <kernel substring> <out.json> [command that made each dir ...]
     python -m paper_2609_10549_amd.profile_summary mfma <counter_dir> <copy_trace_dir> <last_n> <out.md> \
         <job_bytes> <command...>
+    python -m paper_2609_10549_amd.profile_summary counters <out.md> <kernel substring> <title> \
+        <counter_dir>... -- <command of each dir>...
 
 `trace` averages the last `last_n` dispatches of every kernel (the timed
 steps of `bench.py --profile-only`). `traffic` converts the FETCH_SIZE and
@@ -18,7 +20,12 @@ copies grouped into transfer jobs (gaps above 30 us split them). The trace
 holds no sizes: `job_bytes` lists the jobs of one benchmark step as
 bytes:copies pairs, comma-separated; a traced job with one of those copy
 counts is taken to move those bytes in equal parts, and a job with another
-count (a gap that split one) is listed without them."""
+count (a gap that split one) is listed without them. `counters` averages
+every counter of the given runs over the dispatches of one kernel and
+derives utilisations per cycle of the kernel (GRBM_GUI_ACTIVE): LDS active
+(SQ_LDS_IDX_ACTIVE per CU), LDS bank-conflict stalls, MFMA busy
+(SQ_VALU_MFMA_BUSY_CYCLES per SIMD), the texture address and data units'
+busy cycles (TA_TA_BUSY, TD_TD_BUSY per CU) and the waves' LDS issue wait."""
 from __future__ import annotations
 
 import csv
@@ -149,8 +156,74 @@ def mfma(counter_dir, copy_dir, last_n, out, job_bytes, command):
         f.write("\n".join(lines) + "\n")
 
 
+CU_NUM = 256
+SIMD_NUM = 4 * CU_NUM
+XCC_NUM = 8
+SE_NUM = 32
+
+
+def _dispatch_means(dirs, kernel_sub):
+    """{counter: mean per dispatch} over every run directory, for the
+    dispatches whose kernel name contains kernel_sub; `duration_us` is the
+    mean dispatch duration of the first directory (each run perturbs it)."""
+    acc = defaultdict(lambda: defaultdict(float))
+    dur = {}
+    for i, d in enumerate(dirs):
+        for path in glob.glob(os.path.join(d, "*counter_collection.csv")):
+            for r in csv.DictReader(open(path)):
+                if kernel_sub in r["Kernel_Name"]:
+                    acc[r["Counter_Name"]][(d, r["Dispatch_Id"])] += float(r["Counter_Value"])
+                    if i == 0 and "Start_Timestamp" in r:
+                        dur[r["Dispatch_Id"]] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    out = {k: sum(v.values()) / len(v) for k, v in acc.items() if v}
+    if dur:
+        out["duration_us"] = sum(dur.values()) / len(dur)
+    return out
+
+
+def counters(out, kernel_sub, title, dirs, commands):
+    m = _dispatch_means(dirs, kernel_sub)
+    lines = [f"# {title}", "", "Commands:", ""] + [f"* `{c}`" for c in commands] + [
+        "", f"Kernel: dispatches whose name contains `{kernel_sub}`; every counter averaged per dispatch.", "",
+        "| counter | mean per dispatch |", "|---|---|"]
+    for k in sorted(m):
+        lines.append(f"| `{k}` | {m[k]:.4g} |")
+    # GRBM_GUI_ACTIVE comes summed over the 8 XCDs: per-XCD kernel cycles
+    # (rocprof's own MfmaUtil / LdsUtil take the per-XCD maximum)
+    gui = m.get("GRBM_GUI_ACTIVE", 0.0) / XCC_NUM
+    if gui:
+        der = []
+        if "SQ_LDS_IDX_ACTIVE" in m:
+            der.append(("LDS indexed-access active (SQ_LDS_IDX_ACTIVE / (GRBM_GUI_ACTIVE x CUs))", m["SQ_LDS_IDX_ACTIVE"] / (gui * CU_NUM)))
+        if "SQ_LDS_BANK_CONFLICT" in m:
+            der.append(("LDS bank-conflict stall (SQ_LDS_BANK_CONFLICT / (GRBM_GUI_ACTIVE x CUs))",
+                        m["SQ_LDS_BANK_CONFLICT"] / (gui * CU_NUM)))
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+            der.append(("MFMA busy (SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))",
+                        m["SQ_VALU_MFMA_BUSY_CYCLES"] / (gui * SIMD_NUM)))
+        if "TA_TA_BUSY_sum" in m:
+            der.append(("texture address busy (TA_TA_BUSY / (GRBM_GUI_ACTIVE x CUs))", m["TA_TA_BUSY_sum"] / (gui * CU_NUM)))
+        if "TD_TD_BUSY_sum" in m:
+            der.append(("texture data busy (TD_TD_BUSY / (GRBM_GUI_ACTIVE x CUs))", m["TD_TD_BUSY_sum"] / (gui * CU_NUM)))
+        if "SQ_BUSY_CYCLES" in m and m.get("duration_us"):
+            der.append(("shader clock, GHz (SQ_BUSY_CYCLES per shader engine / kernel time)",
+                        m["SQ_BUSY_CYCLES"] / SE_NUM / (m["duration_us"] * 1e3)))
+        if "SQ_WAIT_INST_LDS" in m and "SQ_BUSY_CYCLES" in m:
+            der.append(("wave-cycles waiting to issue LDS per busy cycle (SQ_WAIT_INST_LDS x 4 / SQ_BUSY_CYCLES)",
+                        4 * m["SQ_WAIT_INST_LDS"] / m["SQ_BUSY_CYCLES"]))
+        if der:
+            lines += ["", "Derived, per cycle of the kernel:", "", "| quantity | value |", "|---|---|"]
+            lines += [f"| {name} | {v:.3f} |" for name, v in der]
+    lines += ["", f"Kernel source hash: {kernel_source_hash()}"]
+    with open(out, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
-    if sys.argv[1] == "trace":
+    if sys.argv[1] == "counters":
+        sep = sys.argv.index("--")
+        counters(sys.argv[2], sys.argv[3], sys.argv[4], sys.argv[5:sep], sys.argv[sep + 1:])
+    elif sys.argv[1] == "trace":
         trace(sys.argv[2], int(sys.argv[3]), sys.argv[4], " ".join(sys.argv[5:]))
     elif sys.argv[1] == "mfma":
         mfma(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))

@@ -138,6 +138,34 @@ def test_ag_gemm_integer_exact_all_ranks(ring, n):
         assert np.array_equal(host_bits(case.C), ref), f"rank {r}"
 
 
+@pytest.mark.parametrize("rank,ring", [(3, "double"), (6, "single")])
+def test_ag_gemm_tail_split_integer_exact(rank, ring):
+    # two waves of 256 x 256 tiles at K = 8192: the fused AllGather takes the
+    # larger tile, and the tiles of the last two arriving partitions split K
+    # (4 slices of 2048, summed in slice order); NaN-filled output, paced 4:1
+    n = 8
+    M, N, K = 8192, 4096 + 8, 8192
+    inp = make_int_ag_inputs(M, N, K, n, seed=31 + rank)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    _say("ag tail split", rank, ring, M, N, K)
+    case = AGCase(inp, rank, ring)
+    case.C.fill_(0x7FC0)
+    C.compass_set_option(C.OPT_TILE_TRACE, 8192)
+    try:
+        C.compass_ag_gemm(case.problem, C.links(400e9, 100e9))
+        C.compass_sync()
+        rec = C.compass_tile_trace(8192)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    # 32 x 17 tiles of 256 x 256; the last two row-tile groups (one
+    # partition each) split K: double ring, 512-row partitions, 2 x 2 x 17
+    # tiles in 4 slices; single ring, 1024-row partitions, 2 x 4 x 17 tiles
+    # in 3 slices (the 256 workgroups over a group's 68 tiles)
+    extra = 68 * 3 if ring == "double" else 136 * 2
+    assert len(rec) == 32 * 17 + extra
+    assert np.array_equal(host_bits(case.C), ref)
+
+
 def test_ag_gemm_config1_all_ranks():
     # AllGather-GEMM, TP=2: shards 256x512 U[-1,1], B 512x1024, single ring
     inp = make_ag_inputs(512, 1024, 512, 2, seed=1, dist_a=("uniform", -1.0, 1.0), dist_w=("uniform", -1.0, 1.0))
