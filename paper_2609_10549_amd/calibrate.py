@@ -8,9 +8,9 @@ Measures, through the C ABI only:
   * InterDecom times at d = 2..16 with the GEMM-alone and transfer-alone
     times of the same workload                     -> eta(d) = alpha + beta d
   * fused (IntraFusion) times with the same base   -> overhead alpha_f + beta_f m
-and fits them with compass_calibrate. The shapes come from the Table IV grid
-(those that fit one GPU's share at TP = 8), so the fit never uses the exact
-evaluation workloads of the benchmark.
+and fits them with compass_calibrate. The shapes are one TP = 8 rank's share
+of Table IV workloads at evaluation scale (M >= 4096), disjoint from the
+study's and the benchmark's workloads.
 """
 from __future__ import annotations
 
@@ -27,14 +27,20 @@ from . import compass as C
 HERE = os.path.dirname(os.path.abspath(__file__))
 DEFAULT_OUT = os.path.join(HERE, "calibration.json")
 
-# (pattern, M, N, K, n): Table IV values of M, N, K at TP = 8
+# (pattern, M, N, K, n): one TP = 8 rank's share of Table IV workloads at
+# evaluation scale (M >= 4096): AllGather M x N_int/8 x H, ReduceScatter
+# M x H x N_int/8, with (N_int, H) in {(8192, 8192), (16384, 16384),
+# (4096, 16384)}. None of them is a shape of the model and selector study
+# (its (N_int, H) pairs are (8192, 4096), (16384, 4096), (16384, 8192)) or of
+# the benchmark's workloads, so every evaluation of the fitted model is out
+# of sample.
 SHAPES = [
-    ("ag", 2048, 2048, 4096, 8), ("ag", 4096, 4096, 4096, 8), ("ag", 8192, 4096, 8192, 8),
-    ("ag", 12288, 2048, 8192, 8), ("ag", 16384, 2048, 4096, 8),
-    ("rs", 2048, 4096, 2048, 8), ("rs", 4096, 8192, 2048, 8), ("rs", 12288, 4096, 4096, 8),
-    ("rs", 16384, 8192, 2048, 8),
+    ("ag", 4096, 1024, 8192, 8), ("ag", 16384, 1024, 8192, 8), ("ag", 8192, 2048, 16384, 8),
+    ("ag", 8192, 512, 16384, 8),
+    ("rs", 4096, 8192, 1024, 8), ("rs", 16384, 8192, 1024, 8), ("rs", 8192, 16384, 2048, 8),
+    ("rs", 8192, 16384, 512, 8),
 ]
-QUICK = [SHAPES[0], SHAPES[2], SHAPES[5], SHAPES[7]]
+QUICK = [SHAPES[0], SHAPES[2], SHAPES[4], SHAPES[6]]
 
 
 def _rand_bits(shape, gen):

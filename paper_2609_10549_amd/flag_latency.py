@@ -18,9 +18,10 @@ the same signalling path:
 
 (host start seen - host flag q) + (GPU gate pass of q - GPU first ticket)
 equals d_start + d_flag(q) exactly, whatever the clocks' offset, so each
-partition with a tile that waited at its gate (its gate wait above
-`min_wait_us`) gives that sum, an upper bound of its flag latency. Reported:
-the sums per partition and their median and maximum."""
+partition with a tile that had taken its ticket before the flag was stored
+and waited at the gate (its gate wait above `min_wait_us`) gives that sum, an
+upper bound of its flag latency. Reported: the sums per partition and their
+median and maximum; --keep copies the two raw traces to a directory."""
 from __future__ import annotations
 
 import argparse
@@ -77,11 +78,16 @@ def analyse(copy_csv: str, tiles: np.ndarray, min_wait_us: float = 5.0, tile_row
     part = (rt * bm) // half                      # double ring: partition = 2 c + h = row // (M / 2n)
     out = {}
     for q, t_flag in sorted(flags.items()):
-        m = (part == q) & ((gate - tick) / 100.0 > min_wait_us)
+        host_us = (start_seen - t_flag) * 1e6
+        # tiles of q that began waiting before the flag was stored: a tile's
+        # ticket at GPU time t (relative to the first ticket) happened before
+        # the store when t + host_us < d_start, so t + host_us < 0 is a safe
+        # test whatever d_start >= 0 is; they also waited at the gate
+        began = (tick - first_tick) / 100.0 + host_us < 0.0
+        m = (part == q) & began & ((gate - tick) / 100.0 > min_wait_us)
         if not m.any():
             continue
         gpu_us = (gate[m].min() - first_tick) / 100.0
-        host_us = (start_seen - t_flag) * 1e6
         out[q] = round(gpu_us + host_us, 2)
     s = np.array(list(out.values()))
     return {"epoch": epoch, "sum_us_by_partition": out, "partitions": len(out),
@@ -92,6 +98,7 @@ def analyse(copy_csv: str, tiles: np.ndarray, min_wait_us: float = 5.0, tile_row
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=None)
+    ap.add_argument("--keep", default=None, help="directory to keep the raw copy-side and tile traces in")
     ap.add_argument("--child", default=None, help=argparse.SUPPRESS)
     args = ap.parse_args()
     if args.child:
@@ -106,6 +113,11 @@ def main():
         if rc != 0:
             raise SystemExit(f"child failed with status {rc}")
         res = analyse(trace_csv, np.load(tiles_npy))
+        if args.keep:
+            import shutil
+            os.makedirs(args.keep, exist_ok=True)
+            shutil.copy(trace_csv, os.path.join(args.keep, "flag_latency_copy.csv"))
+            shutil.copy(tiles_npy, os.path.join(args.keep, "flag_latency_tiles.npy"))
     res.update(shape=[M, N, K, n], rates_Bps=list(RATES))
     print(json.dumps(res, indent=1))
     if args.out:

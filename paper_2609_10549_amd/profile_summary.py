@@ -1,10 +1,10 @@
 """Summarise rocprofv3 CSV output into the text kept under profiles/.
 
     python -m paper_2609_10549_amd.profile_summary trace <kernel_trace.csv> <last_n> <out.md> <command...>
-    python -m paper_2609_10549_amd.profile_summary traffic <fetch_dir> <write_dir> <copy_fetch_dir> \
+    python -m paper_2609_10549_amd.profile_summary traffic [--last=N] <fetch_dir> <write_dir> <copy_fetch_dir> \
         <copy_write_dir> <kernel substring> <out.json> [command that made each dir ...]
     python -m paper_2609_10549_amd.profile_summary mfma <counter_dir> <copy_trace_dir> <last_n> <out.md> \
-        <job_bytes> <command...>
+        "<kernel>:<bytes>;..." <command...>
     python -m paper_2609_10549_amd.profile_summary counters <out.md> <kernel substring> <title> \
         <counter_dir>... -- <command of each dir>...
 
@@ -15,12 +15,10 @@ each scaled by what the same counter reads for a plain 256 MiB copy kernel,
 and records a hash of the kernel source the counters were taken with. `mfma`
 reports MfmaUtil (matrix-core busy cycles over active cycles of every SIMD)
 and the bf16 MFMA work of every GEMM kernel, averaged over its last `last_n`
-dispatches, and the SDMA side from a memory-copy trace: device-to-device
-copies grouped into transfer jobs (gaps above 30 us split them). The trace
-holds no sizes: `job_bytes` lists the jobs of one benchmark step as
-bytes:copies pairs, comma-separated; a traced job with one of those copy
-counts is taken to move those bytes in equal parts, and a job with another
-count (a gap that split one) is listed without them. `counters` averages
+dispatches, with the shader clock, and the SDMA side from a memory-copy
+trace: device-to-device copies attributed to the operator whose GEMM
+dispatch window they start in, the bytes of each operator given by its
+kernel name. `counters` averages
 every counter of the given runs over the dispatches of one kernel and
 derives utilisations per cycle of the kernel (GRBM_GUI_ACTIVE): LDS active
 (SQ_LDS_IDX_ACTIVE per CU), LDS bank-conflict stalls, MFMA busy
@@ -72,9 +70,13 @@ def _counter(d, name, kernel_sub):
     return [vals[k] for k in sorted(vals, key=int)]
 
 
-def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, kernel_sub, out, *commands):
+def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, kernel_sub, out, *commands, last_n=0):
+    """HBM bytes per launch of kernel_sub (its last `last_n` dispatches if
+    positive: the timed steps)."""
     fk = _counter(fetch_dir, "FETCH_SIZE", kernel_sub)
     wk = _counter(write_dir, "WRITE_SIZE", kernel_sub)
+    if last_n > 0:
+        fk, wk = fk[-last_n:], wk[-last_n:]
     cf = _counter(cfetch_dir, "FETCH_SIZE", "copy")
     cw = _counter(cwrite_dir, "WRITE_SIZE", "copy")
     # the copy reads and writes COPY_BYTES per dispatch
@@ -93,65 +95,74 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, kernel_sub, out, *comm
 
 
 
-def mfma(counter_dir, copy_dir, last_n, out, job_bytes, command):
-    kinds = {int(c): int(b) for b, c in (x.split(":") for x in job_bytes.split(","))}
+def mfma(counter_dir, copy_dir, last_n, out, op_bytes, command):
+    """MfmaUtil of the GEMM kernels (last `last_n` dispatches each) and the
+    SDMA copies of the last `last_n` operators. `copy_dir` holds a memory-copy
+    trace and a kernel trace of the same run; every copy is attributed to the
+    operator whose GEMM dispatch window it starts in (from that dispatch's
+    start to the next GEMM dispatch's start: the copy side starts after the
+    kernel's first workgroup, and stream order puts the next operator's
+    kernel after this one's copies). `op_bytes` maps a GEMM kernel name to
+    the bytes its operator moves, as name:bytes pairs separated by ";"."""
+    sizes = dict(x.rsplit(":", 1) for x in op_bytes.split(";"))
+    sizes = {k: int(v) for k, v in sizes.items()}
     by = defaultdict(lambda: defaultdict(list))
     for path in glob.glob(os.path.join(counter_dir, "*counter_collection.csv")):
         for r in csv.DictReader(open(path)):
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
             by[r["Kernel_Name"].split("(")[0].replace("void ", "")][r["Counter_Name"]].append(
-                (int(r["Dispatch_Id"]), float(r["Counter_Value"])))
-    lines = ["# Matrix-core utilisation and SDMA copy rates, bench.py --profile-only", "",
+                (int(r["Dispatch_Id"]), float(r["Counter_Value"]), dur))
+    lines = ["# Matrix-core utilisation and SDMA copies, timed steps of bench.py --profile-only", "",
              f"Command: `{command}`", "",
-             f"GEMM kernels, last {last_n} dispatches each (MfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs / "
-             "(GRBM_GUI_ACTIVE x SIMDs)):", "",
-             "| kernel | dispatches | MfmaUtil % | bf16 MFMA GFLOP per dispatch |", "|---|---|---|---|"]
+             f"GEMM kernels, last {last_n} dispatches each. MfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs / "
+             "(GRBM_GUI_ACTIVE x SIMDs); the shader clock is SQ_BUSY_CYCLES per shader engine over the dispatch "
+             "duration:", "",
+             "| kernel | dispatches | avg us | MfmaUtil % | shader clock GHz | bf16 MFMA GFLOP per dispatch |",
+             "|---|---|---|---|---|---|"]
     for name, d in sorted(by.items()):
         if "gemm_kernel" not in name:
             continue
-        util = [v for _, v in sorted(d["MfmaUtil"])][-last_n:]
-        mops = [v for _, v in sorted(d["SQ_INSTS_VALU_MFMA_MOPS_BF16"])][-last_n:]
-        lines.append(f"| `{name}` | {len(util)} | {sum(util) / len(util):.1f} | "
-                     f"{sum(mops) / len(mops) * 512 / 1e9:.1f} |")
+        util = sorted(d["MfmaUtil"])[-last_n:]
+        mops = sorted(d["SQ_INSTS_VALU_MFMA_MOPS_BF16"])[-last_n:]
+        busy = sorted(d.get("SQ_BUSY_CYCLES", []))[-last_n:]
+        avg_us = sum(x[2] for x in util) / len(util)
+        clk = (sum(x[1] for x in busy) / len(busy) / SE_NUM / (avg_us * 1e3)) if busy else float("nan")
+        lines.append(f"| `{name}` | {len(util)} | {avg_us:.1f} | {sum(x[1] for x in util) / len(util):.1f} | "
+                     f"{clk:.2f} | {sum(x[1] for x in mops) / len(mops) * 512 / 1e9:.1f} |")
     copies = []
     for path in glob.glob(os.path.join(copy_dir, "*memory_copy_trace.csv")):
         for r in csv.DictReader(open(path)):
             if r["Direction"].endswith("DEVICE_TO_DEVICE"):
                 copies.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
     copies.sort()
-    jobs, cur = [], []
-    for c in copies:
-        if cur and c[0] - max(e for _, e in cur) > 30_000:
-            jobs.append(cur)
-            cur = []
-        cur.append(c)
-    if cur:
-        jobs.append(cur)
-    tail = jobs[-last_n:]
-    per_kind = defaultdict(list)
-    for j in tail:
-        if len(j) in kinds:
-            per_kind[len(j)].extend((e - b) / 1e3 for b, e in j)
-    lines += ["", f"SDMA device-to-device copies: {len(copies)} in {len(jobs)} transfer jobs; the last {len(tail)} "
-              "jobs:", ""]
-    for ncopy, v in kinds.items():
-        dur = sorted(per_kind.get(ncopy, []))
-        if not dur:
-            continue
-        size = v / ncopy
+    gemms = []
+    for path in glob.glob(os.path.join(copy_dir, "*kernel_trace.csv")):
+        for r in csv.DictReader(open(path)):
+            if "gemm_kernel" in r["Kernel_Name"]:
+                gemms.append((int(r["Start_Timestamp"]), r["Kernel_Name"].split("(")[0].replace("void ", "")))
+    gemms.sort()
+    ops = []
+    for i, (t0, name) in enumerate(gemms):
+        t1 = gemms[i + 1][0] if i + 1 < len(gemms) else float("inf")
+        cs = [c for c in copies if t0 <= c[0] < t1]
+        if cs and name in sizes:
+            ops.append((name, cs))
+    tail = ops[-last_n:]
+    lines += ["", f"SDMA device-to-device copies of the last {len(tail)} operators (each attributed to its GEMM "
+              "dispatch window); per-copy durations are the engines' own, the span runs from the operator's "
+              "first copy start to its last copy end:", "",
+              "| operator kernel | MiB moved | copies | copy p10 / p50 / p90 us | span us | aggregate GB/s |",
+              "|---|---|---|---|---|---|"]
+    for name, cs in tail:
+        dur = sorted((e - b) / 1e3 for b, e in cs)
         pct = lambda q: dur[min(len(dur) - 1, int(q * len(dur)))]  # noqa: E731
-        lines.append(f"* jobs of {v / 2**20:.0f} MiB in {ncopy} copies of {size / 2**20:.2f} MiB: duration "
-                     f"p10 / p50 / p90 = {pct(0.1):.1f} / {pct(0.5):.1f} / {pct(0.9):.1f} us, "
-                     f"i.e. {size / pct(0.5) / 1e3:.1f} GB/s per copy at the median")
-    lines += ["", "The memory-copy tracer intercepts every copy call on the host, which stretches a job's "
-              "span against an untraced run (the benchmark's own transfer-alone times are the reference); the "
-              "per-copy durations are the engines' own.", "",
-              "| job | MiB | copies | span us | aggregate GB/s |", "|---|---|---|---|---|"]
-    for i, j in enumerate(tail):
-        span = (max(e for _, e in j) - min(b for b, _ in j)) / 1e3
-        v = kinds.get(len(j))
-        mib, rate = (f"{v / 2**20:.0f}", f"{v / span / 1e3:.1f}") if v else ("?", "?")
-        lines.append(f"| {i} | {mib} | {len(j)} | {span:.1f} | {rate} |")
-    lines += ["", f"Kernel source hash: {kernel_source_hash()}"]
+        span = (max(e for _, e in cs) - min(b for b, _ in cs)) / 1e3
+        v = sizes[name]
+        lines.append(f"| `{name}` | {v / 2**20:.0f} | {len(cs)} | {pct(0.1):.1f} / {pct(0.5):.1f} / {pct(0.9):.1f} | "
+                     f"{span:.1f} | {v / span / 1e3:.1f} |")
+    lines += ["", "The memory-copy tracer intercepts every copy call on the host, which stretches a span against "
+              "an untraced run (the benchmark's own transfer-alone times are the reference).", "",
+              f"Kernel source hash: {kernel_source_hash()}"]
     with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
 
@@ -228,4 +239,9 @@ if __name__ == "__main__":
     elif sys.argv[1] == "mfma":
         mfma(sys.argv[2], sys.argv[3], int(sys.argv[4]), sys.argv[5], sys.argv[6], " ".join(sys.argv[7:]))
     else:
-        traffic(*sys.argv[2:])
+        args = sys.argv[2:]
+        last = 0
+        if args and args[0].startswith("--last="):
+            last = int(args[0].split("=", 1)[1])
+            args = args[1:]
+        traffic(*args, last_n=last)

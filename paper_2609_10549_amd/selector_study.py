@@ -27,7 +27,8 @@ Reported:
     slowdown of its picks;
   * the same MAE, d* regret and selector accuracy with the model refitted on
     half of the study's workloads and evaluated on the other half (two-fold
-    cross-validation), i.e. calibrated for this workload range.
+    cross-validation), and refitted on all workloads but the evaluated one
+    (leave one workload out), i.e. calibrated for this workload range.
 The model inputs are the measured GEMM-alone and transfer-alone times, so the
 errors are those of the overhead models. Timing only (seeded random bf16).
 """
@@ -178,6 +179,7 @@ def cross_validated(points, folds: int = 2) -> dict:
     keys = sorted({json.dumps(p["w"], sort_keys=True) for p in points})
     fold_of = {k: i % folds for i, k in enumerate(keys)}
     aw, fu, correct, regret, fits = [], [], 0, [], []
+    aw_by_d = {}
     for f in range(folds):
         train = [p for p in points if fold_of[json.dumps(p["w"], sort_keys=True)] != f]
         test = [p for p in points if fold_of[json.dumps(p["w"], sort_keys=True)] == f]
@@ -189,8 +191,10 @@ def cross_validated(points, folds: int = 2) -> dict:
                                    K=p["w"]["K"], n=p["w"]["n"])
             for k, v in p["t_decomp"].items():
                 if k != "1":
-                    aw.append(abs(C.compass_model_t_decomp(p["t_gemm"], p["t_xfer"], int(k), cal.alpha_decomp,
-                                                           cal.beta_decomp) - v))
+                    e = abs(C.compass_model_t_decomp(p["t_gemm"], p["t_xfer"], int(k), cal.alpha_decomp,
+                                                     cal.beta_decomp) - v)
+                    aw.append(e)
+                    aw_by_d.setdefault(k, []).append(e)
             step = p["t_xfer"] / (p["w"]["n"] - 1)
             fu.append(abs(C.compass_model_t_fusion(w, p["t_gemm"], step, cal.alpha_fusion, cal.beta_fusion)
                           - p["t_fused"]))
@@ -225,6 +229,7 @@ def cross_validated(points, folds: int = 2) -> dict:
         fc += list(np.abs(te[:, 1] + c0 * te[:, 0] - te[:, 2]))
         fits[f]["fixed_cost_per_subop_us"] = 1e6 * c0
     return dict(folds=folds, fits=fits, decomp_mae_aware_us=1e6 * float(np.mean(aw)),
+                decomp_mae_aware_by_d_us={k: 1e6 * float(np.mean(v)) for k, v in sorted(aw_by_d.items(), key=lambda kv: int(kv[0]))},
                 decomp_mae_fixed_cost_us=1e6 * float(np.mean(fc)),
                 fusion_mae_aware_us=1e6 * float(np.mean(fu)), selector_accuracy=correct / len(points),
                 mean_regret_dstar=float(np.mean(regret)))
@@ -259,6 +264,8 @@ def main():
                 points += json.load(f)
     summary = summarize(points)
     summary["cross_validated"] = cross_validated(points)
+    n_work = len({json.dumps(p["w"], sort_keys=True) for p in points})
+    summary["leave_one_out"] = cross_validated(points, folds=n_work)
     print(json.dumps(summary, indent=1), flush=True)
     if args.out:
         with open(args.out, "w") as f:

@@ -23,12 +23,12 @@ def test_bench_refuses_more_than_one_gpu():
 def test_stored_traffic_follows_the_kernel_source(monkeypatch):
     import bench
     from paper_2609_10549_amd import profile_summary as PS
-    with open(os.path.join(ROOT, "profiles", "traffic_rs.json")) as f:
+    with open(os.path.join(ROOT, "profiles", "traffic_gpt3_rs.json")) as f:
         rec = json.load(f)
     monkeypatch.setattr(PS, "kernel_source_hash", lambda: rec["kernel_source_hash"])
-    assert bench.stored_traffic("rs") == round(rec["traffic_bytes_per_launch"], 0)
+    assert bench.stored_traffic("gpt3_rs") == round(rec["traffic_bytes_per_launch"], 0)
     monkeypatch.setattr(PS, "kernel_source_hash", lambda: "0" * 16)
-    assert bench.stored_traffic("rs") is None
+    assert bench.stored_traffic("gpt3_rs") is None
     assert bench.stored_traffic("no_such_kernel") is None
 
 
@@ -56,34 +56,38 @@ def test_trace_summary_averages_the_last_dispatches(tmp_path):
     assert f"Kernel source hash: {PS.kernel_source_hash()}" in text
 
 
-def test_copy_summary_classifies_jobs_by_copy_count(tmp_path):
+def test_copy_summary_attributes_copies_to_operator_windows(tmp_path):
     from paper_2609_10549_amd import profile_summary as PS
     cdir = tmp_path / "counters"
     cdir.mkdir()
-    _write(cdir / "b_counter_collection.csv", ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"],
-           [[1, "void compass::gemm_kernel<128, 128, true>(x)", "MfmaUtil", 20.0],
-            [1, "void compass::gemm_kernel<128, 128, true>(x)", "SQ_INSTS_VALU_MFMA_MOPS_BF16", 2.0e9 / 512]])
+    k = "void compass::gemm_kernel<128, 128, true>(x)"
+    # 1 ms dispatch, 20 % busy matrix cores, 2 GFLOP, 2.0e6 busy cycles per SE -> 2.0 GHz
+    _write(cdir / "b_counter_collection.csv",
+           ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"],
+           [[1, k, "MfmaUtil", 20.0, 0, 1_000_000],
+            [1, k, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 2.0e9 / 512, 0, 1_000_000],
+            [1, k, "SQ_BUSY_CYCLES", 2.0e6 * PS.SE_NUM, 0, 1_000_000]])
     tdir = tmp_path / "copies"
     tdir.mkdir()
-    rows = []
-    t = 0
-    # a job of 2 copies of 1 MiB each 10 us, a job of 4 copies each 20 us, a job of 3 (unknown)
-    for n, dur in ((2, 10_000), (4, 20_000), (3, 5_000)):
-        for _ in range(n):
-            rows.append(["MEMORY_COPY", "MEMORY_COPY_DEVICE_TO_DEVICE", t, t + dur])
-            t += 1_000
-        t += 100_000   # a gap that separates the jobs
+    ag = "void compass::gemm_kernel<256, 256, false>(compass::GemmParams)"
+    rs = "void compass::gemm_kernel<256, 256, true>(compass::GemmParams)"
+    # two operators: the AllGather window [0, 100 us) with 2 copies of 10 us,
+    # the ReduceScatter window from 100 us with 3 copies of 20 us
+    _write(tdir / "b_kernel_trace.csv", ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+           [[ag, 0, 90_000], [rs, 100_000, 190_000], ["join_kernel", 190_000, 200_000]])
+    rows = [["MEMORY_COPY", "MEMORY_COPY_DEVICE_TO_DEVICE", t, t + 10_000] for t in (5_000, 20_000)]
+    rows += [["MEMORY_COPY", "MEMORY_COPY_DEVICE_TO_DEVICE", t, t + 20_000] for t in (110_000, 115_000, 180_000)]
+    rows += [["MEMORY_COPY", "MEMORY_COPY_HOST_TO_DEVICE", 1_000, 2_000]]
     _write(tdir / "b_memory_copy_trace.csv", ["Kind", "Direction", "Start_Timestamp", "End_Timestamp"], rows)
     out = tmp_path / "m.md"
-    PS.mfma(str(cdir), str(tdir), 20, str(out), f"{2 << 20}:2,{8 << 20}:4", "cmd")
+    PS.mfma(str(cdir), str(tdir), 20, str(out),
+            f"compass::gemm_kernel<256, 256, false>:{2 << 20};compass::gemm_kernel<256, 256, true>:{6 << 20}", "cmd")
     text = out.read_text()
-    assert "| `compass::gemm_kernel<128, 128, true>` | 1 | 20.0 | 2.0 |" in text
-    assert "jobs of 2 MiB in 2 copies of 1.00 MiB: duration p10 / p50 / p90 = 10.0 / 10.0 / 10.0 us" in text
-    assert "jobs of 8 MiB in 4 copies of 2.00 MiB" in text
-    table = [ln for ln in text.splitlines() if ln.startswith("| 0 ") or ln.startswith("| 1 ") or ln.startswith("| 2 ")]
-    assert table[0].startswith("| 0 | 2 | 2 | 11.0 |")    # span 0 .. 11 us
-    assert table[1].startswith("| 1 | 8 | 4 | 23.0 |")
-    assert table[2] == "| 2 | ? | 3 | 7.0 | ? |"
+    assert "| `compass::gemm_kernel<128, 128, true>` | 1 | 1000.0 | 20.0 | 2.00 | 2.0 |" in text
+    # AllGather: 2 copies spanning 5 .. 30 us = 25 us, 2 MiB -> 83.9 GB/s
+    assert "| `compass::gemm_kernel<256, 256, false>` | 2 | 2 | 10.0 / 10.0 / 10.0 | 25.0 | 83.9 |" in text
+    # ReduceScatter: 3 copies spanning 110 .. 200 us = 90 us, 6 MiB -> 69.9 GB/s
+    assert "| `compass::gemm_kernel<256, 256, true>` | 6 | 3 | 20.0 / 20.0 / 20.0 | 90.0 | 69.9 |" in text
 
 
 def test_traffic_summary_scales_by_the_copy_probe(tmp_path):
