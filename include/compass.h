@@ -211,7 +211,13 @@ int compass_partition_layout(int pattern, int ring, int n, int rank, int M, cons
  *     (device or pinned host, (M/n) x N bf16) receives chunk c of C as soon
  *     as all of its tiles are stored — the emulated send to the next rank.
  *
- * Unused fields of the other pattern may be NULL. */
+ * Unused fields of the other pattern may be NULL. Size limits: K and N
+ * multiples of 8; M at most 65536 (the row-tile table); the kernel addresses
+ * a tile's operands with 32-bit offsets from the tile's first row of A and
+ * of the partial (its first column of W), so a 256-row tile may span at most
+ * 1 GiB of each: K <= 2^21 and, for the ReduceScatter, N <= 2^20 (InterDecom
+ * with d > 1: the row pieces a tile covers, a chunk apart, within the same
+ * 1 GiB). Operands may exceed 4 GiB. Beyond these: COMPASS_ERR_UNSUPPORTED. */
 typedef struct compass_problem {
     int pattern;
     int M, N, K;
@@ -259,7 +265,8 @@ int compass_decomp_gemm(const compass_problem *p, int d, const compass_links *li
  * compass_gemm: the same GEMM kernel with nothing to wait for (T_gemm).
  *   A: device M x K bf16, W: device N x K bf16, C: device M x N bf16,
  *   P: NULL or device M x N fp32 added before rounding. Same size limits as
- *   a compass_problem (K, N multiples of 8; A and W at most 1 GiB).
+ *   a compass_problem (K, N multiples of 8; M at most 65536; a 256-row tile
+ *   of A, W and P within 1 GiB, i.e. K <= 2^21 and, with P, N <= 2^20).
  * compass_transfer: exactly the copies the fused operator of `p` issues, at
  *   the same pacing, with no GEMM (T_xfer); a one-workgroup kernel on the
  *   stream starts the copies and ends when the last one landed.
@@ -286,7 +293,7 @@ int compass_sequential(const compass_problem *p, const compass_links *links, voi
  * overlap on one GPU (concurrent streams) race on the shared scratch; issue
  * them on one stream. Errors: COMPASS_ERR_INVALID for a bad shape or NULL
  * operand, COMPASS_ERR_UNSUPPORTED beyond the size limits (M above the
- * 65536 rows of the tile table, A or W above 1 GiB, M x N fp32 above 2 GiB)
+ * 65536 rows of the tile table, K above 2^21, N above 2^20 with P)
  * or on a device other than gfx950, COMPASS_ERR_HIP when a launch fails;
  * all before anything is enqueued except the last. */
 int compass_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C,

@@ -17,6 +17,7 @@ constexpr int kTraceWords = 8;       // words per tile-trace record
 constexpr int kCuSlots = 8 * 256;    // ctrl words: per (XCC, SE/SH/CU id) slot claims
 constexpr int kMaxSplitTiles = 512;  // tiles of a split-K launch (one counter each)
 constexpr int kMaxSplit = 16;        // K slices per tile
+constexpr uint64_t kTileSpanMax = 1ull << 30;   // bytes of A, W or P one tile may span
 
 // Tile configurations of the GEMM kernel.
 enum TileCfg : int {
@@ -39,9 +40,13 @@ struct GemmParams {
     const uint16_t *W;   // bf16, N x K
     uint16_t *C;         // bf16 output, rows addressed through the row map
     const float *P;      // fp32 partial added before rounding (or null)
-    uint32_t a_bytes;    // extent of A in bytes (buffer bound)
-    uint32_t w_bytes;    // extent of W in bytes
-    uint32_t p_bytes;    // extent of P in bytes (buffer bound of the partial loads)
+    // extents in bytes; a tile's buffer loads are bounded by them, from a
+    // base at the tile's first row of A and P (its first column of W), with
+    // 32-bit offsets from there (the host keeps each tile's span of A, W and
+    // P below kTileSpanMax)
+    uint64_t a_bytes;
+    uint64_t w_bytes;
+    uint64_t p_bytes;
     int M, N, K;         // logical rows of this launch, columns, depth
     int lda, ldw, ldc, ldp;
     int tiles_m, tiles_n;

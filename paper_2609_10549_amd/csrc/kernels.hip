@@ -46,10 +46,22 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_AS(p) ((__attribute__((address_space(3))) void *)(p))
 
-// Offset added for an out-of-range row or K column: A and W are at most
-// 1 GiB each, so a row offset plus a column offset (either possibly kOOB)
-// stays below 2^32 and lands beyond the buffer bound whenever either is kOOB.
-constexpr uint32_t kOOB = 0x40000000u;
+// Buffer loads of a tile go through a resource based at the tile's first
+// row (A, the partial) or first column (W), bounded by the bytes left in the
+// operand, at most kTileSpanMax; offsets are relative to that base. An
+// out-of-range row or column takes an offset at or beyond the bound:
+// kOOBRow = 2^31 for a row, kOOBCol = 2^30 for a K column. A valid row offset
+// plus a valid column offset stays below the 2^30 bound (the host checks the
+// tile's span), a valid one plus an out-of-range one reaches it, and two
+// out-of-range ones sum to 3 * 2^30, below 2^32, so no sum wraps.
+constexpr uint32_t kOOBRow = 0x80000000u;
+constexpr uint32_t kOOBCol = 0x40000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void *base, uint64_t total, uint64_t off) {
+    const uint64_t left = total > off ? total - off : 0;
+    const uint32_t bound = (uint32_t)(left < kTileSpanMax ? left : kTileSpanMax);
+    return __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)base + off), (short)0, (int)bound, 0x00020000);
+}
 
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -304,8 +316,6 @@ void gemm_kernel(const GemmParams p) {
     const int total = p.split_from + (p.tiles_m * p.tiles_n - p.split_from) * p.ksplit;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
-    const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void *)p.A, (short)0, (int)p.a_bytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc((void *)p.W, (short)0, (int)p.w_bytes, 0x00020000);
 
     // loader geometry: load q of this wave covers tile rows 32 q + 8 wave +
     // (lane >> 3), 128 bytes (K = 64) each; the lane loads the logical chunk
@@ -381,17 +391,21 @@ void gemm_kernel(const GemmParams p) {
 
         {   // a timed-out tile still runs (its loads stay in bounds); only its
             // stores are dropped
+            // A from the tile's first (mapped) row, W from its first column
+            const int row0 = map_row(p, m0);
+            const __amdgpu_buffer_rsrc_t rA = tile_rsrc(p.A, p.a_bytes, (uint64_t)row0 * (uint64_t)p.lda * 2u);
+            const __amdgpu_buffer_rsrc_t rW = tile_rsrc(p.W, p.w_bytes, (uint64_t)n0 * (uint64_t)p.ldw * 2u);
             uint32_t offA[NOFF], offW[NOFF];
 #pragma unroll
             for (int q = 0; q < NOFF; ++q) {
                 const int ia = m0 + 32 * q + lrow0;
-                offA[q] = ia < p.M ? (uint32_t)map_row(p, ia) * (uint32_t)p.lda * 2u : kOOB;
+                offA[q] = ia < p.M ? (uint32_t)(map_row(p, ia) - row0) * (uint32_t)p.lda * 2u : kOOBRow;
                 const int iw = n0 + 32 * q + lrow0;
-                offW[q] = iw < p.N ? (uint32_t)iw * (uint32_t)p.ldw * 2u : kOOB;
+                offW[q] = iw < p.N ? (uint32_t)(iw - n0) * (uint32_t)p.ldw * 2u : kOOBRow;
             }
             auto kcol = [&](int st) -> uint32_t {   // byte offset of this lane's K chunk in stage st
                 const int kc = kb + st * kBK + cchunk * 8;
-                return kc < ke ? (uint32_t)kc * 2u : kOOB;
+                return kc < ke ? (uint32_t)kc * 2u : kOOBCol;
             };
             // an even stage count keeps the unrolled loop free of early exits
             // (padding stages read only out-of-range columns, i.e. zeros)
@@ -574,8 +588,9 @@ void gemm_kernel(const GemmParams p) {
                 // buffers; loading it into registers one block at a time
                 // would expose a memory latency per block)
                 constexpr int NB = FM * FN;
+                const int prow0 = map_row(p, m0);
                 const __amdgpu_buffer_rsrc_t rP =
-                    __builtin_amdgcn_make_buffer_rsrc((void *)p.P, (short)0, (int)p.p_bytes, 0x00020000);
+                    tile_rsrc(p.P, p.p_bytes, (uint64_t)prow0 * (uint64_t)p.ldp * 4u);
                 const int rr = lane >> 3, rc = lane & 7;
                 char *pbuf0 = sA1 + wave * 4096;
                 char *pbuf1 = sW0 + wave * 4096;
@@ -586,8 +601,8 @@ void gemm_kernel(const GemmParams p) {
                     for (int it = 0; it < 4; ++it) {
                         const int m = m0 + wm0 + mi * 32 + rr + 8 * it;
                         const uint32_t off = (m < p.M && n < p.N)
-                                                 ? ((uint32_t)map_row(p, m) * (uint32_t)p.ldp + (uint32_t)n) * 4u
-                                                 : 0x80000000u;
+                                                 ? ((uint32_t)(map_row(p, m) - prow0) * (uint32_t)p.ldp + (uint32_t)n) * 4u
+                                                 : kOOBRow;
                         __builtin_amdgcn_raw_ptr_buffer_load_lds(rP, LDS_AS(dst + it * 1024), 16, off, 0, 0, 0);
                     }
                 };

@@ -94,8 +94,12 @@ int op_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C, 
     if (!A || !W || !C) return set_error(COMPASS_ERR_INVALID, "A, W and C are required");
     if ((M + 127) / 128 > kMaxRowTiles)
         return set_error(COMPASS_ERR_UNSUPPORTED, "M = %d above the %d rows of the tile table", M, kMaxRowTiles * 128);
-    if ((double)M * K * 2 > 1073741824.0 || (double)N * K * 2 > 1073741824.0 || (double)M * N * 4 >= 2147483648.0)
-        return set_error(COMPASS_ERR_UNSUPPORTED, "A or W above 1 GiB, or M x N fp32 above 2 GiB");
+    // the kernel addresses a tile's operands with 32-bit offsets from the
+    // tile's first row (column of W): a 256-row tile spans at most
+    // kTileSpanMax bytes of each
+    if (256ull * (uint64_t)K * 2 > kTileSpanMax || (P && 256ull * (uint64_t)N * 4 > kTileSpanMax))
+        return set_error(COMPASS_ERR_UNSUPPORTED, "K = %d, N = %d: a 256-row tile would span more than 1 GiB of A, W "
+                                                  "or the partial", K, N);
     DeviceScratch d;
     int rc = current_scratch(&d);
     if (rc != COMPASS_OK) return rc;
@@ -117,9 +121,9 @@ int op_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C, 
     g.ldw = K;
     g.ldc = N;
     g.ldp = N;
-    g.a_bytes = (uint32_t)((size_t)M * K * 2);
-    g.w_bytes = (uint32_t)((size_t)N * K * 2);
-    g.p_bytes = P ? (uint32_t)((size_t)M * N * 4) : 0u;
+    g.a_bytes = (uint64_t)M * (uint64_t)K * 2;
+    g.w_bytes = (uint64_t)N * (uint64_t)K * 2;
+    g.p_bytes = P ? (uint64_t)M * (uint64_t)N * 4 : 0u;
     g.tiles_m = (M + bm - 1) / bm;
     g.tiles_n = (N + bn - 1) / bn;
     const int total = g.tiles_m * g.tiles_n;

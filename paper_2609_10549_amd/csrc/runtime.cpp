@@ -1100,6 +1100,14 @@ static int make_geometry(int pattern, int ring, int n, int rank, int M, const co
     return COMPASS_OK;
 }
 
+// Whether a tile whose rows span `span_rows` rows of A (and of the fp32
+// partial, with_p) and 256 columns of W stays within the kernel's 32-bit
+// buffer offsets from its base (kTileSpanMax bytes each).
+static bool spans_fit(int K, int N, bool with_p, uint64_t span_rows) {
+    return span_rows * (uint64_t)K * 2 <= kTileSpanMax && 256ull * (uint64_t)K * 2 <= kTileSpanMax &&
+           (!with_p || span_rows * (uint64_t)N * 4 <= kTileSpanMax);
+}
+
 static int validate(const compass_problem *p, const compass_links *l, int want_pattern, Geometry *g) {
     if (!p) return set_error(COMPASS_ERR_INVALID, "problem is NULL");
     if (!l) return set_error(COMPASS_ERR_INVALID, "links is NULL");
@@ -1109,9 +1117,9 @@ static int validate(const compass_problem *p, const compass_links *l, int want_p
     if (p->N < 1 || p->K < 1) return set_error(COMPASS_ERR_INVALID, "M, N, K must be positive");
     if (p->K % 8 || p->N % 8) return set_error(COMPASS_ERR_INVALID, "K and N must be multiples of 8");
     if ((p->M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
-    if ((double)p->M * p->K * 2 > 1073741824.0 || (double)p->N * p->K * 2 > 1073741824.0 ||
-        (double)p->M * p->N * 4 >= 2147483648.0)
-        return set_error(COMPASS_ERR_UNSUPPORTED, "A or W above 1 GiB, or M x N fp32 above 2 GiB");
+    if (!spans_fit(p->K, p->N, p->pattern == COMPASS_GEMM_RS, 256))
+        return set_error(COMPASS_ERR_UNSUPPORTED, "K = %d, N = %d: a 256-row tile would span more than 1 GiB of A, W "
+                                                  "or the partial", p->K, p->N);
     if (!p->W || !p->C) return set_error(COMPASS_ERR_INVALID, "W and C are required");
     if (p->pattern == COMPASS_AG_GEMM) {
         if (!p->shard_src || !p->gathered) return set_error(COMPASS_ERR_INVALID, "shard_src and gathered are required");
@@ -1216,9 +1224,9 @@ static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A,
     g.M = M; g.N = N; g.K = K;
     g.kslice = K;
     g.lda = K; g.ldw = K; g.ldc = N; g.ldp = N;
-    g.a_bytes = (uint32_t)(a_rows * (size_t)K * 2);
-    g.w_bytes = (uint32_t)((size_t)N * K * 2);
-    g.p_bytes = P ? (uint32_t)(a_rows * (size_t)N * 4) : 0u;
+    g.a_bytes = (uint64_t)a_rows * (uint64_t)K * 2;
+    g.w_bytes = (uint64_t)N * (uint64_t)K * 2;
+    g.p_bytes = P ? (uint64_t)a_rows * (uint64_t)N * 4 : 0u;
     const int bm = tile_rows(cfg), bn = tile_cols(cfg);
     g.tiles_m = (M + bm - 1) / bm;
     g.tiles_n = (N + bn - 1) / bn;
@@ -1880,6 +1888,15 @@ int op_decomp(const compass_problem *p, int d, const compass_links *l, void *str
     if (d > 1 && geo.sub > 1)
         return set_error(COMPASS_ERR_UNSUPPORTED, "InterDecom takes one flag per piece (sub_chunks <= 1)");
     if (d * geo.P > kFinalFlag0) return set_error(COMPASS_ERR_UNSUPPORTED, "d * partitions exceeds the flag slots");
+    if (d > 1) {
+        // a sub-GEMM's tile of 256 logical rows covers up to 255 / piece + 1
+        // row pieces, each a chunk's rows apart in A and the partial
+        const uint64_t piece = (uint64_t)(geo.rows / d);
+        const uint64_t span = (255 / piece + 1) * (uint64_t)geo.rows;
+        if (!spans_fit(p->K, p->N, p->pattern == COMPASS_GEMM_RS, span))
+            return set_error(COMPASS_ERR_UNSUPPORTED, "d = %d: a sub-GEMM tile would span more than 1 GiB of A or the "
+                                                      "partial", d);
+    }
     if ((rc = begin()) != COMPASS_OK) return rc;
     hipStream_t s = (hipStream_t)stream;
     const uint32_t epoch = next_epoch();
@@ -1943,8 +1960,9 @@ int op_gemm(int M, int N, int K, const void *A, const void *W, void *C, const fl
     if (M < 1 || N < 1 || K < 1 || K % 8 || N % 8) return set_error(COMPASS_ERR_INVALID, "need positive M, N, K with K, N multiples of 8");
     if (!A || !W || !C) return set_error(COMPASS_ERR_INVALID, "A, W and C are required");
     if ((M + 127) / 128 > kMaxRowTiles) return set_error(COMPASS_ERR_UNSUPPORTED, "M too large");
-    if ((double)M * K * 2 > 1073741824.0 || (double)N * K * 2 > 1073741824.0 || (double)M * N * 4 >= 2147483648.0)
-        return set_error(COMPASS_ERR_UNSUPPORTED, "A or W above 1 GiB, or M x N fp32 above 2 GiB");
+    if (!spans_fit(K, N, P != nullptr, 256))
+        return set_error(COMPASS_ERR_UNSUPPORTED, "K = %d, N = %d: a 256-row tile would span more than 1 GiB of A, W "
+                                                  "or the partial", K, N);
     int rc = begin();
     if (rc != COMPASS_OK) return rc;
     GemmParams g;

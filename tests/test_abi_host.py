@@ -307,9 +307,11 @@ def test_degenerate_and_oversized_problems_are_refused_before_enqueue(pattern):
         ((64, 64, 60, 2), C.ERR_INVALID),         # K not a multiple of 8
         ((64, 64, 64, 0), C.ERR_INVALID),         # no ranks
         ((128, 64, 64, 33), C.ERR_INVALID),       # more ranks than the flag masks hold
-        ((65536, 64, 8200, 2), C.ERR_UNSUPPORTED),   # A above 1 GiB
-        ((64, 65536, 8200, 2), C.ERR_UNSUPPORTED),   # W above 1 GiB
+        ((65664, 64, 64, 2), C.ERR_UNSUPPORTED),     # M beyond the 65536 rows of the tile table
+        ((64, 64, 2097160, 2), C.ERR_UNSUPPORTED),   # K so deep a 256-row tile spans over 1 GiB of A
     ]
+    if pattern == C.GEMM_RS:   # N so wide a 256-row tile spans over 1 GiB of the fp32 partial
+        cases.append(((64, 1048584, 64, 2), C.ERR_UNSUPPORTED))
     for (M, N, K, n), want in cases:
         st, keep = _fake_problem(pattern, M, N, K, n)
         assert call(ctypes.byref(st), ctypes.byref(lk), None) == want, (M, N, K, n)
@@ -355,7 +357,8 @@ def test_plain_gemm_refuses_degenerate_shapes():
     for M, N, K in ((0, 8, 8), (8, 0, 8), (8, 8, 0), (8, 12, 8), (8, 8, 12)):
         assert lib.compass_gemm(M, N, K, fake, fake, fake, None, None) == C.ERR_INVALID
     assert lib.compass_gemm(8, 8, 8, None, fake, fake, None, None) == C.ERR_INVALID
-    assert lib.compass_gemm(65536, 64, 8200, fake, fake, fake, None, None) == C.ERR_UNSUPPORTED
+    assert lib.compass_gemm(65664, 64, 64, fake, fake, fake, None, None) == C.ERR_UNSUPPORTED      # M
+    assert lib.compass_gemm(64, 64, 2097160, fake, fake, fake, None, None) == C.ERR_UNSUPPORTED    # K
     for it in (0, -1, 1 << 23):
         a, b = ctypes.c_double(), ctypes.c_double()
         assert lib.compass_probe_mfma(it, ctypes.byref(a), ctypes.byref(b)) == C.ERR_INVALID

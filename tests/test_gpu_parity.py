@@ -963,3 +963,38 @@ def test_copy_side_timeout_then_recovers(pool_depth):
     for q in range(n):
         if q != 1:
             assert np.array_equal(host_bits(case.send[q]), rref[q * rows:(q + 1) * rows]), q
+
+
+# ------------------------------------------------------------ operands beyond 1 / 2 GiB
+def test_gemm_rs_two_gib_partial_integer_exact():
+    # Table IV's largest ReduceScatter output, one TP = 4 rank's share (M =
+    # 32768 tokens, hidden 16384): a 2 GiB fp32 landing buffer and a 1 GiB
+    # output; row offsets of the partial pass 2^31 bytes
+    n = 4
+    M, N, K = 32768, 16384, 1024
+    _say("rs 2 GiB partial", M, N, K)
+    inp = make_int_rs_inputs(M, N, K, n, seed=2048)
+    case = RSCase(inp, 1, "single")
+    case.C.fill_(0x7FC0)
+    C.compass_gemm_rs(case.problem, C.links(0.0, 0.0))
+    C.compass_sync()
+    ref = O.f64_to_bf16_rne(case.reference())
+    assert np.array_equal(host_bits(case.C), ref)
+    rows = M // n
+    for q in range(n):
+        if q != 1:
+            assert torch.equal(case.send[q], case.C[q * rows:(q + 1) * rows]), q
+
+
+def test_ag_gemm_gathered_above_one_gib_integer_exact():
+    # a gathered A of 32768 x 20480 bf16 (1.34 GB) over a paced double ring
+    n = 8
+    M, N, K = 32768, 264, 20480
+    _say("ag gathered above 1 GiB", M, N, K)
+    inp = make_int_ag_inputs(M, N, K, n, seed=2049)
+    case = AGCase(inp, 6, "double")
+    case.C.fill_(0x7FC0)
+    C.compass_ag_gemm(case.problem, C.links(200e9, 50e9))
+    C.compass_sync()
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    assert np.array_equal(host_bits(case.C), ref)

@@ -80,4 +80,6 @@ def test_noalloc_gemm_rejects_sizes_before_touching_the_device():
     assert lib.compass_gemm_noalloc(65537, 64, 64, 16, 16, 16, None, None) == C.ERR_UNSUPPORTED
     assert lib.compass_gemm_noalloc(64, 64, 60, 16, 16, 16, None, None) == C.ERR_INVALID
     assert lib.compass_gemm_noalloc(64, 64, 64, None, 16, 16, None, None) == C.ERR_INVALID
-    assert lib.compass_gemm_noalloc(40000, 8, 16384, 16, 16, 16, None, None) == C.ERR_UNSUPPORTED   # A > 1 GiB
+    # a 256-row tile spanning over 1 GiB of A (K) or of the fp32 partial (N)
+    assert lib.compass_gemm_noalloc(64, 64, 2097160, 16, 16, 16, None, None) == C.ERR_UNSUPPORTED
+    assert lib.compass_gemm_noalloc(64, 1048584, 64, 16, 16, 16, 16, None) == C.ERR_UNSUPPORTED
