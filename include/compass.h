@@ -342,6 +342,20 @@ int compass_sync(void);
                                        of k per item, the widest k whose groups carry the
                                        link rate with this many per cent to spare (0..100,
                                        default 5); wider groups land each item sooner */
+#define COMPASS_OPT_TAIL_MIN_K   13 /* fused AllGather with 256 x 256 tiles: from this K
+                                       on, the tiles of the last COMPASS_OPT_TAIL_GROUPS
+                                       row-tile groups of the ready order (the last
+                                       arrivals) split K into at most 4 slices, each at
+                                       least COMPASS_OPT_TAIL_SLICE_K deep, as many as the
+                                       workgroup slots over one group's tiles; fp32
+                                       partial tiles in the split-K workspace (default
+                                       8192; 0 = never; at most 2^21) */
+#define COMPASS_OPT_TAIL_MIN_K_128 14 /* the same for 128 x 128 tiles (default 0 = never) */
+#define COMPASS_OPT_TAIL_SLICE_K 15 /* least K depth of a tail slice, a positive multiple
+                                       of 64 (default 2048) */
+#define COMPASS_OPT_TAIL_GROUPS  16 /* row-tile groups the tail split covers, 1..8
+                                       (default 2); none when the launch has fewer than
+                                       twice as many groups */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

@@ -41,6 +41,10 @@ OPT_TILE_TRACE = 8
 OPT_SCHED = 9
 OPT_POOL = 10
 OPT_PACE_HEADROOM = 12
+OPT_TAIL_MIN_K = 13
+OPT_TAIL_MIN_K_128 = 14
+OPT_TAIL_SLICE_K = 15
+OPT_TAIL_GROUPS = 16
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RING_DOUBLE_SPLIT = 2

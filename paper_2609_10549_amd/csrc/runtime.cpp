@@ -174,6 +174,11 @@ struct Ctx {
     int tile_override = 0;           // 0 auto, 1 256 x 256, 2 128 x 128
     int pool_depth = kDefaultPoolDepth;   // unpaced directions share the engines (0: split)
     double pace_headroom = 0.05;          // paced groups: throughput to spare over the link rate
+    // fused AllGather tail split: K depth from which it applies (per tile
+    // shape, 0: never), least slice depth, row-tile groups it covers
+    int tail_min_k[2] = {kTailMinK, 0};   // [0] 256 x 256, [1] 128 x 128
+    int tail_slice_k = kTailSliceK;
+    int tail_groups = 2;
     // optional HIP events around every GEMM launch (kernel durations)
     bool timing = false;
     static constexpr int kTimed = 512;
@@ -1283,13 +1288,14 @@ static void set_split(GemmParams &g, int cfg) {
 // latency dwarfs the partial tiles' round trip through the workspace.
 static void set_tail_split(GemmParams &g, int cfg) {
     Ctx &c = g_ctx;
-    if (!(c.sched & kSchedSplitK) || !c.split_ws || g.ksplit > 1 || g.K < kTailMinK) return;
+    const int min_k = c.tail_min_k[cfg == kTile256 ? 0 : 1];
+    if (!(c.sched & kSchedSplitK) || !c.split_ws || g.ksplit > 1 || min_k <= 0 || g.K < min_k) return;
     const int groups = (g.tiles_m + g.group_m - 1) / g.group_m;
-    if (groups < 4 || g.tiles_m % g.group_m) return;
-    const int tail_groups = 2;
+    const int tail_groups = c.tail_groups;
+    if (groups < 2 * tail_groups || g.tiles_m % g.group_m) return;
     const int tail_tiles = tail_groups * g.group_m * g.tiles_n;
     const int slots = g.grid;
-    int sp = std::min(4, std::min(slots / (g.group_m * g.tiles_n), g.K / kTailSliceK));
+    int sp = std::min(4, std::min(slots / (g.group_m * g.tiles_n), g.K / c.tail_slice_k));
     const size_t tile_bytes = (size_t)tile_rows(cfg) * tile_cols(cfg) * sizeof(float);
     while (sp > 1 && (size_t)tail_tiles * sp * tile_bytes > c.split_ws_bytes) --sp;
     if (sp < 2 || tail_tiles > kMaxSplitTiles) return;
@@ -1817,7 +1823,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     double arrive[2 * kMaxRanks];
     if ((rc = expected_arrivals(p, geo, l, resident_mask(p, geo), arrive)) != COMPASS_OK) return rc;
     order_by_arrival(g, cfg, geo, p->M, true, arrive);
-    if (cfg == kTile256) set_tail_split(g, cfg);
+    set_tail_split(g, cfg);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
@@ -2125,6 +2131,20 @@ int op_set_option(int key, long long v) {
     case COMPASS_OPT_SCHED:
         if (v < 0 || v > 7) return set_error(COMPASS_ERR_INVALID, "schedule option must be in [0, 7]");
         c.sched = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_TAIL_MIN_K:
+    case COMPASS_OPT_TAIL_MIN_K_128:
+        if (v < 0 || v > (1 << 21)) return set_error(COMPASS_ERR_INVALID, "tail split depth out of range");
+        c.tail_min_k[key == COMPASS_OPT_TAIL_MIN_K ? 0 : 1] = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_TAIL_SLICE_K:
+        if (v < 64 || v > (1 << 21) || v % 64) return set_error(COMPASS_ERR_INVALID, "tail slice depth must be a "
+                                                                 "positive multiple of 64");
+        c.tail_slice_k = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_TAIL_GROUPS:
+        if (v < 1 || v > 8) return set_error(COMPASS_ERR_INVALID, "tail groups must lie in [1, 8]");
+        c.tail_groups = (int)v;
         return COMPASS_OK;
     case COMPASS_OPT_DROP_FLAG:
         if (v < -1 || v >= 2 * kMaxRanks) return set_error(COMPASS_ERR_INVALID, "drop flag out of range");

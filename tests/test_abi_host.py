@@ -394,3 +394,21 @@ def test_binding_checks_shapes_element_sizes_and_contiguity():
                      0, "single")
     with pytest.raises(ValueError, match="entries"):
         C.rs_problem(i16(M, K), i16(N, K), parts, f32(M, N), i16(M, N), sends[:2], 0, "single")
+
+
+def test_tail_split_options_are_validated_without_a_gpu():
+    # host-side options: set and refused without touching the device
+    lib = C.lib()
+    good = [(C.OPT_TAIL_MIN_K, 0), (C.OPT_TAIL_MIN_K, 8192), (C.OPT_TAIL_MIN_K_128, 4096),
+            (C.OPT_TAIL_MIN_K_128, 0), (C.OPT_TAIL_SLICE_K, 1024), (C.OPT_TAIL_SLICE_K, 2048),
+            (C.OPT_TAIL_GROUPS, 1), (C.OPT_TAIL_GROUPS, 2)]
+    for k, v in good:
+        assert lib.compass_set_option(k, v) == C.OK, (k, v)
+    bad = [(C.OPT_TAIL_MIN_K, -1), (C.OPT_TAIL_MIN_K, (1 << 21) + 1), (C.OPT_TAIL_MIN_K_128, -5),
+           (C.OPT_TAIL_SLICE_K, 0), (C.OPT_TAIL_SLICE_K, 1000), (C.OPT_TAIL_GROUPS, 0), (C.OPT_TAIL_GROUPS, 9)]
+    for k, v in bad:
+        assert lib.compass_set_option(k, v) == C.ERR_INVALID, (k, v)
+    # back to the defaults
+    for k, v in [(C.OPT_TAIL_MIN_K, 8192), (C.OPT_TAIL_MIN_K_128, 0), (C.OPT_TAIL_SLICE_K, 2048),
+                 (C.OPT_TAIL_GROUPS, 2)]:
+        assert lib.compass_set_option(k, v) == C.OK

@@ -163,3 +163,37 @@ def test_flag_latency_pairs_the_two_clocks(tmp_path):
     assert res["epoch"] == 7
     assert res["partitions"] == 1
     assert abs(res["sum_us_by_partition"][3] - (44.0 - 400.0)) < 1e-6
+
+
+def test_tile_timeline_splits_item_time(tmp_path):
+    # double ring, M = 64, n = 2: partitions of 16 rows, 16-row tiles;
+    # host: start seen at 5.0 s, flag 2 at +30 us, flag 3 at +50 us, the
+    # send gate of partition 2 opened at +80 us
+    import numpy as np
+    from paper_2609_10549_amd import tile_timeline as TT
+    path = tmp_path / "copy.csv"
+    _write(path, ["t_s", "role", "epoch", "event", "item", "bytes"],
+           [[1.0, 0, 3, "start_seen", -1, 0], [5.0, 0, 4, "start_seen", -1, 0],
+            [5.00003, 0, 4, "flag", 2, 0], [5.00005, 1, 4, "flag", 3, 0], [5.00008, 2, 4, "gate_open", 2, 0]])
+
+    def rec(rt, tick, gate, loop, end):
+        return [0, rt << 16, 0, 0, tick, gate, loop, end]
+
+    # AllGather: tile of row tile 2 (partition 2) waits 1000 -> 4000 ticks,
+    # computes to 5000, epilogue to 5500; the others never wait
+    t = np.array([rec(0, 1000, 1000, 2000, 2100), rec(1, 1000, 1000, 2000, 2100),
+                  rec(2, 1000, 4000, 5000, 5500), rec(3, 1200, 6000, 7000, 7200)], dtype=np.uint32)
+    r = TT.analyse(str(path), t, "ag", 64, 2, "double", tile_rows=16)
+    assert r["span_us"] == 62.0 and r["last_flag_us"] == 50.0 and r["tail_after_last_flag_us"] == 12.0
+    p2 = [p for p in r["partitions"] if p["partition"] == 2][0]
+    assert p2["flag_us"] == 30.0 and p2["first_gate_us"] == 30.0 and p2["wait_us"] == 30.0
+    assert p2["main_us"] == 10.0 and p2["epilogue_us"] == 5.0 and p2["last_end_us"] == 45.0
+    tot = 11 + 11 + 45 + 60
+    assert abs(r["share_wait"] - round((30 + 48) / tot, 3)) < 1e-9
+    assert r["last_step"]["partitions"] == [2, 3] and r["last_step"]["last_end_us"] == 62.0
+    # ReduceScatter: the gate is the epilogue's, after the main loop
+    t = np.array([rec(2, 1000, 5000, 3000, 5200)], dtype=np.uint32)
+    r = TT.analyse(str(path), t, "rs", 64, 2, "double", tile_rows=16)
+    p = r["partitions"][0]
+    assert p["main_us"] == 20.0 and p["wait_us"] == 20.0 and p["epilogue_us"] == 2.0
+    assert p["send_start_us"] == 80.0
