@@ -185,8 +185,11 @@ int compass_partition_layout(int pattern, int ring, int n, int rank, int M, cons
  * The emulated rank r owns row chunk r, rows [r*M/n, (r+1)*M/n).
  *
  * Requirements: 1 <= n <= 32, 0 <= rank < n, M % n == 0 (and M % (2n) == 0
- * for the double ring), K % 8 == 0, N % 8 == 0, M*K*2 and N*K*2 at most
- * 2^30 bytes, M*N*4 below 2^31 bytes, M / 128 rounded up at most 512.
+ * for the double ring), K % 8 == 0, N % 8 == 0, and the size limits below.
+ * Every range a copy engine reads or writes (a shard, a partial, a send
+ * chunk, their rows of gathered / partial_stage / C) must lie inside the
+ * allocation that holds its first byte, as the HSA runtime reports it:
+ * otherwise COMPASS_ERR_INVALID, before anything is enqueued.
  *
  * AllGather + GEMM (pattern COMPASS_AG_GEMM):
  *   shard_src[q], q = 0..n-1: (M/n) x K bf16 shard of rank q. shard_src[rank]

@@ -198,7 +198,7 @@ struct Ctx {
     std::mutex trace_mu;
     std::vector<std::string> trace;
     struct Range { uintptr_t lo, hi; hsa_agent_t owner; };
-    std::vector<Range> ranges;       // pointer -> owning agent cache
+    std::vector<Range> ranges;       // allocations looked up by the current call (owner, bounds)
     ~Ctx();
 };
 
@@ -365,11 +365,17 @@ static int ensure_init() {
 }
 
 // Owning agent of a pointer (device memory -> GPU, host memory -> CPU).
-static int agent_of(const void *ptr, hsa_agent_t *out) {
+// The agent owning the allocation that holds `ptr`, and the end of that
+// allocation (*end, optional).
+static int agent_of(const void *ptr, hsa_agent_t *out, uintptr_t *end = nullptr) {
     Ctx &c = g_ctx;
     const uintptr_t u = (uintptr_t)ptr;
     for (auto &r : c.ranges)
-        if (u >= r.lo && u < r.hi) { *out = r.owner; return COMPASS_OK; }
+        if (u >= r.lo && u < r.hi) {
+            *out = r.owner;
+            if (end) *end = r.hi;
+            return COMPASS_OK;
+        }
     hsa_amd_pointer_info_t info;
     std::memset(&info, 0, sizeof info);
     info.size = sizeof info;
@@ -386,6 +392,7 @@ static int agent_of(const void *ptr, hsa_agent_t *out) {
     if (c.ranges.size() > 256) c.ranges.clear();
     c.ranges.push_back({lo, lo + info.sizeInBytes, owner});
     *out = owner;
+    if (end) *end = lo + info.sizeInBytes;
     return COMPASS_OK;
 }
 
@@ -1391,10 +1398,17 @@ int op_partition_layout(int pattern, int ring, int n, int rank, int M, const com
     return g.P;
 }
 
+// A copy of `bytes` from src to dst; both ranges must lie inside the
+// allocations that hold their first bytes (so that a buffer smaller than
+// the problem says is refused before a copy engine writes past it).
 static int make_item(Item *it, void *dst, const void *src, size_t bytes, int flag, int gate) {
     int rc;
-    if ((rc = agent_of(dst, &it->dst_agent)) != COMPASS_OK) return rc;
-    if ((rc = agent_of(src, &it->src_agent)) != COMPASS_OK) return rc;
+    uintptr_t dst_end = 0, src_end = 0;
+    if ((rc = agent_of(dst, &it->dst_agent, &dst_end)) != COMPASS_OK) return rc;
+    if ((rc = agent_of(src, &it->src_agent, &src_end)) != COMPASS_OK) return rc;
+    if ((uintptr_t)dst + bytes > dst_end || (uintptr_t)src + bytes > src_end)
+        return set_error(COMPASS_ERR_INVALID, "a copy of %zu bytes from %p to %p runs past the end of its allocation",
+                         bytes, src, dst);
     it->dst = dst;
     it->src = src;
     it->bytes = bytes;
@@ -1757,6 +1771,9 @@ static int join(uint32_t epoch, const std::vector<int> &flags, bool write_start,
 static int begin(void) {
     int rc = ensure_init();
     if (rc != COMPASS_OK) return rc;
+    // allocations seen by an earlier call may have been freed and their
+    // addresses reused by others (of another size or owner) since
+    g_ctx.ranges.clear();
     return take_async_error();
 }
 
