@@ -90,6 +90,7 @@ constexpr int kMinSliceK = 512;      // K depth of a slice at least
 constexpr int kSplitWsTiles = 2;     // workspace: this many 256 x 256 fp32 partial tiles per CU
 constexpr int kTailMinK = 8192;      // fused AllGather: split the tail's K from this depth on
 constexpr int kTailSliceK = 2048;    // ... into slices at least this deep, at most 4
+constexpr double kTailMaxLambda = 2.0;   // ... when the estimated comp / comm ratio is below this
 // host_words layout (pinned, coherent host memory): start word, error word,
 // done flags (kernel -> copy side), arrival flags (copy side -> kernel)
 constexpr int kHwStart = 0, kHwErr = 1, kHwDone = 64, kHwFlags = kHwDone + kMaxFlags;
@@ -1292,11 +1293,18 @@ static void set_split(GemmParams &g, int cfg) {
 // (one partition each) split K into s slices, s = the workgroup slots over a
 // group's tiles, at most 4, each at least kTailSliceK deep; the rest of the
 // launch runs whole tiles. Only for K >= kTailMinK, where a whole tile's
-// latency dwarfs the partial tiles' round trip through the workspace.
-static void set_tail_split(GemmParams &g, int cfg) {
+// latency dwarfs the partial tiles' round trip through the workspace, and
+// only when the transfer is not much shorter than the GEMM (estimated
+// lambda below kTailMaxLambda): with the data there early the last tiles
+// start with the rest, and the slices' round trips are pure cost (GPT-3
+// AllGather, 4 : 1 ring: lambda ~ 0.7 split 1474 against 1616 us whole,
+// lambda ~ 1 1117 against 1185 us; lambda ~ 2 split 1091 against 1038 us,
+// links unpaced 1074 against 1024 us).
+static void set_tail_split(GemmParams &g, int cfg, double lam_est) {
     Ctx &c = g_ctx;
     const int min_k = c.tail_min_k[cfg == kTile256 ? 0 : 1];
     if (!(c.sched & kSchedSplitK) || !c.split_ws || g.ksplit > 1 || min_k <= 0 || g.K < min_k) return;
+    if (!(lam_est < kTailMaxLambda)) return;
     const int groups = (g.tiles_m + g.group_m - 1) / g.group_m;
     const int tail_groups = c.tail_groups;
     if (groups < 2 * tail_groups || g.tiles_m % g.group_m) return;
@@ -1830,8 +1838,8 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     init_params(g, epoch);
     // (rate-proportional parts: a 256-row tile may span both parts of a
     // chunk and waits for the later one, which an AllGather tolerates)
-    const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 && geo.sub == 1 ? geo.rows : min_part_rows(geo),
-                              lambda_estimate(p, geo, l));
+    const double lam = lambda_estimate(p, geo, l);
+    const int cfg = pick_tile(p->M, p->N, true, geo.fb != 0.5 && geo.sub == 1 ? geo.rows : min_part_rows(geo), lam);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->gathered, p->M, p->W, p->C, nullptr)) != COMPASS_OK) return rc;
     // 256-row tiles: one row-tile group per partition, so that the dealing
     // and the tail split follow partitions
@@ -1840,7 +1848,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     double arrive[2 * kMaxRanks];
     if ((rc = expected_arrivals(p, geo, l, resident_mask(p, geo), arrive)) != COMPASS_OK) return rc;
     order_by_arrival(g, cfg, geo, p->M, true, arrive);
-    set_tail_split(g, cfg);
+    set_tail_split(g, cfg, lam);
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);

@@ -164,6 +164,18 @@ def test_ag_gemm_tail_split_integer_exact(rank, ring):
     extra = 68 * 3 if ring == "double" else 136 * 2
     assert len(rec) == 32 * 17 + extra
     assert np.array_equal(host_bits(case.C), ref)
+    # links unpaced (the engines' ceiling): the transfer is far shorter than
+    # the GEMM (estimated comp / comm ratio above 2), so no tile splits
+    case.C.fill_(0x7FC0)
+    C.compass_set_option(C.OPT_TILE_TRACE, 8192)
+    try:
+        C.compass_ag_gemm(case.problem, C.links(0.0, 0.0))
+        C.compass_sync()
+        rec = C.compass_tile_trace(8192)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    assert len(rec) == 32 * 17
+    assert np.array_equal(host_bits(case.C), ref)
 
 
 def test_ag_gemm_config1_all_ranks():
