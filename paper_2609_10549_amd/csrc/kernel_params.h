@@ -40,13 +40,15 @@ struct GemmParams {
     const uint16_t *W;   // bf16, N x K
     uint16_t *C;         // bf16 output, rows addressed through the row map
     const float *P;      // fp32 partial added before rounding (or null)
-    // extents in bytes; a tile's buffer loads are bounded by them, from a
-    // base at the tile's first row of A and P (its first column of W), with
-    // 32-bit offsets from there (the host keeps each tile's span of A, W and
-    // P below kTileSpanMax)
+    // extents in bytes; a tile's buffer loads (and, with a partial, its
+    // stores of C) are bounded by them, from a base at the tile's first row
+    // of A, P and C (its first column of W), with 32-bit offsets from there
+    // (the host keeps each tile's span of A, W and P below kTileSpanMax; C's
+    // rows are half as wide as P's)
     uint64_t a_bytes;
     uint64_t w_bytes;
     uint64_t p_bytes;
+    uint64_t c_bytes;
     int M, N, K;         // logical rows of this launch, columns, depth
     int lda, ldw, ldc, ldp;
     int tiles_m, tiles_n;

@@ -1,6 +1,6 @@
 // gfx950 kernels of the Compass hot path.
 //
-// gemm_kernel<BM, BN, RS>: persistent bf16 GEMM, C = A * W^T with fp32
+// gemm_kernel<BM, BN, RS, WT>: persistent bf16 GEMM, C = A * W^T with fp32
 // accumulation on the CDNA4 matrix cores (v_mfma_f32_32x32x16_bf16) and one
 // bf16 round-to-nearest-even store. Workgroups take BM x BN output tiles from
 // atomic ticket queues in the order the host chose (ring-arrival order for
@@ -43,6 +43,7 @@ namespace compass {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 #define LDS_AS(p) ((__attribute__((address_space(3))) void *)(p))
 
@@ -292,8 +293,10 @@ __device__ __forceinline__ void stage2e(char *cA, char *cW, char *nA, char *nW, 
 }
 
 // RS = false: optional main-loop gate (AllGather), plain store.
-// RS = true: optional epilogue gate, fp32 partial add, chunk-done signalling.
-template <int BM, int BN, bool RS>
+// RS = true: optional epilogue gate, fp32 partial add, chunk-done signalling;
+// WT = true (a launch whose finished chunks the copy engines send on): the
+// partial-add epilogue stores every tile with system-scope write-through.
+template <int BM, int BN, bool RS, bool WT = false>
 __global__ __launch_bounds__(kThreads, BM == 256 ? 1 : 2)
 void gemm_kernel(const GemmParams p) {
     constexpr int WM = BM / 2, WN = BN / 2;
@@ -583,17 +586,39 @@ void gemm_kernel(const GemmParams p) {
                     finish_split(std::integral_constant<int, BB / 2>{}, std::integral_constant<int, kMaxSplit>{});
             } else if (has_p) {
                 // as through_patch, with each 32 x 32 block's fp32 partial
-                // brought into LDS by buffer_load ... lds one block ahead of
-                // its use (two 4 KiB buffers per wave in the freed stage
-                // buffers; loading it into registers one block at a time
-                // would expose a memory latency per block)
+                // brought into LDS by buffer_load ... lds two blocks ahead of
+                // its use, into three 4 KiB buffers per wave, one in each of
+                // the freed stage buffers sA1, sW0 and sW1. C goes out through
+                // buffer stores that the buffer bound drops for rows or
+                // columns outside C (or all of a failed tile), so every block
+                // issues the same memory operations and the wait for a
+                // block's partial lets the two later blocks' loads and the
+                // stores in between stay in flight (with one block ahead, or
+                // with stores skipped by a branch, it waited for all of them:
+                // the epilogue took 17 us per 256 x 256 tile at any number of
+                // workgroups, against 7 us without a partial)
                 constexpr int NB = FM * FN;
+                constexpr int NSLOT = 3, AHEAD = NSLOT - 1;
                 const int prow0 = map_row(p, m0);
                 const __amdgpu_buffer_rsrc_t rP =
                     tile_rsrc(p.P, p.p_bytes, (uint64_t)prow0 * (uint64_t)p.ldp * 4u);
                 const int rr = lane >> 3, rc = lane & 7;
-                char *pbuf0 = sA1 + wave * 4096;
-                char *pbuf1 = sW0 + wave * 4096;
+                char *const pslot[NSLOT] = {sA1 + wave * 4096, sW0 + wave * 4096, sW1 + wave * 4096};
+                const __amdgpu_buffer_rsrc_t rC =
+                    tile_rsrc(p.C, p.c_bytes, (uint64_t)prow0 * (uint64_t)p.ldc * 2u);
+                auto store_c = [&](int row, int col, float v0, float v1, float v2, float v3) {
+                    const int m = m0 + row, n = n0 + col;
+                    const uint32_t off = (m < mlim && n < p.N)
+                                             ? ((uint32_t)(map_row(p, m) - prow0) * (uint32_t)p.ldc + (uint32_t)n) * 2u
+                                             : kOOBRow;
+                    const u32x2 o = {pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+                    // (a per-tile choice would be a branch around each store,
+                    // which the compiler cannot count)
+                    if constexpr (WT)   // sc0 sc1: written through to memory, the copy engines read it
+                        __builtin_amdgcn_raw_buffer_store_b64(o, rC, off, 0, 17);
+                    else
+                        __builtin_amdgcn_raw_buffer_store_b64(o, rC, off, 0, 0);
+                };
                 auto load_p = [&](int blk, char *dst) {
                     const int mi = blk / FN, ni = blk % FN;
                     const int n = n0 + wn0 + ni * 32 + 4 * rc;
@@ -606,11 +631,13 @@ void gemm_kernel(const GemmParams p) {
                         __builtin_amdgcn_raw_ptr_buffer_load_lds(rP, LDS_AS(dst + it * 1024), 16, off, 0, 0, 0);
                     }
                 };
-                load_p(0, pbuf0);
+#pragma unroll
+                for (int blk = 0; blk < AHEAD && blk < NB; ++blk) load_p(blk, pslot[blk]);
 #pragma unroll
                 for (int blk = 0; blk < NB; ++blk) {
-                    char *pcur = (blk & 1) ? pbuf1 : pbuf0;
-                    if (blk + 1 < NB) load_p(blk + 1, (blk & 1) ? pbuf0 : pbuf1);
+                    char *pcur = pslot[blk % NSLOT];
+                    // into the slot of block blk - 1, whose reads ended the last iteration
+                    if (blk + AHEAD < NB) load_p(blk + AHEAD, pslot[(blk + AHEAD) % NSLOT]);
                     const int mi = blk / FN, ni = blk % FN;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
@@ -625,8 +652,8 @@ void gemm_kernel(const GemmParams p) {
                         const int row = rr + 8 * it;
                         const f32x4 x = *reinterpret_cast<const f32x4 *>(patch + row * 128 + ((rc ^ (row & 7)) << 4));
                         const f32x4 pv = *reinterpret_cast<const f32x4 *>(pcur + row * 128 + rc * 16);
-                        store4(wm0 + mi * 32 + row, wn0 + ni * 32 + 4 * rc, x[0] + pv[0], x[1] + pv[1],
-                               x[2] + pv[2], x[3] + pv[3], false);
+                        store_c(wm0 + mi * 32 + row, wn0 + ni * 32 + 4 * rc, x[0] + pv[0], x[1] + pv[1],
+                                x[2] + pv[2], x[3] + pv[3]);
                     }
                     __builtin_amdgcn_s_waitcnt(0xC07F);   // patch and partial read before reuse
                 }
@@ -744,11 +771,19 @@ hipError_t launch_mfma_probe(uint64_t *out, int grid, int iters, hipStream_t str
 
 hipError_t launch_gemm(const GemmParams &p, int cfg, bool rs, hipStream_t stream) {
     if (cfg == kTile256) {
-        if (rs) hipLaunchKernelGGL((gemm_kernel<256, 256, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
-        else hipLaunchKernelGGL((gemm_kernel<256, 256, false>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        if (rs && p.done_host)
+            hipLaunchKernelGGL((gemm_kernel<256, 256, true, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        else if (rs)
+            hipLaunchKernelGGL((gemm_kernel<256, 256, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        else
+            hipLaunchKernelGGL((gemm_kernel<256, 256, false>), dim3(p.grid), dim3(kThreads), 0, stream, p);
     } else {
-        if (rs) hipLaunchKernelGGL((gemm_kernel<128, 128, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
-        else hipLaunchKernelGGL((gemm_kernel<128, 128, false>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        if (rs && p.done_host)
+            hipLaunchKernelGGL((gemm_kernel<128, 128, true, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        else if (rs)
+            hipLaunchKernelGGL((gemm_kernel<128, 128, true>), dim3(p.grid), dim3(kThreads), 0, stream, p);
+        else
+            hipLaunchKernelGGL((gemm_kernel<128, 128, false>), dim3(p.grid), dim3(kThreads), 0, stream, p);
     }
     return hipGetLastError();
 }

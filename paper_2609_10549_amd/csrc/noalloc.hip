@@ -124,6 +124,7 @@ int op_gemm_noalloc(int M, int N, int K, const void *A, const void *W, void *C, 
     g.a_bytes = (uint64_t)M * (uint64_t)K * 2;
     g.w_bytes = (uint64_t)N * (uint64_t)K * 2;
     g.p_bytes = P ? (uint64_t)M * (uint64_t)N * 4 : 0u;
+    g.c_bytes = (uint64_t)M * (uint64_t)N * 2;
     g.tiles_m = (M + bm - 1) / bm;
     g.tiles_n = (N + bn - 1) / bn;
     const int total = g.tiles_m * g.tiles_n;

@@ -1240,6 +1240,7 @@ static int set_shape(GemmParams &g, int cfg, int M, int N, int K, const void *A,
     g.a_bytes = (uint64_t)a_rows * (uint64_t)K * 2;
     g.w_bytes = (uint64_t)N * (uint64_t)K * 2;
     g.p_bytes = P ? (uint64_t)a_rows * (uint64_t)N * 4 : 0u;
+    g.c_bytes = (uint64_t)a_rows * (uint64_t)N * 2;
     const int bm = tile_rows(cfg), bn = tile_cols(cfg);
     g.tiles_m = (M + bm - 1) / bm;
     g.tiles_n = (N + bn - 1) / bn;
