@@ -331,16 +331,21 @@ int compass_sync(void);
                                        fewer tiles than half the workgroup slots split K
                                        (fp32 partial tiles in a library workspace of
                                        CUs x 256 KiB, summed in slice order) */
-#define COMPASS_OPT_POOL        10  /* unpaced links with more than one active direction
-                                       (double ring; ReduceScatter incoming and outgoing):
-                                       > 0 = the directions share every copy engine, each
-                                       engine with at most this many copies queued, slices
-                                       taken in transfer order (an outgoing sum right after
-                                       its partition's incoming partial) from items that are
-                                       ready, in slices of 3 MiB unless the links set
-                                       slice_bytes; 0 = the engines split per direction in
-                                       proportion to their bytes (default 4: queued copies
-                                       hide the copy side's reaction time; at most 8) */
+#define COMPASS_OPT_POOL        10  /* operators whose copies all stay in device memory
+                                       (not the AlltoAll pattern): > 0 = every ring
+                                       direction, incoming and outgoing, shares every copy
+                                       engine, each engine with at most this many copies
+                                       queued; an engine with room takes the next slice of
+                                       the ready item with the earliest due time (unpaced:
+                                       due at once, transfer order; paced: when its link,
+                                       carrying one item at a time at its rate, would have
+                                       delivered it), and a paced item's flag waits for its
+                                       due time; slices of 2 MiB paced, 3 MiB unpaced,
+                                       unless the links set slice_bytes; 0 = the engines
+                                       split per direction in proportion to their bytes
+                                       (default 4: queued copies hide the copy side's
+                                       reaction time; at most 8). Copies to or from host
+                                       memory always keep a job per direction. */
 #define COMPASS_OPT_PACE_HEADROOM 12 /* paced links: the engines of a direction form groups
                                        of k per item, the widest k whose groups carry the
                                        link rate with this many per cent to spare (0..100,
