@@ -357,7 +357,10 @@ int compass_sync(void);
                                        least COMPASS_OPT_TAIL_SLICE_K deep, as many as the
                                        workgroup slots over one group's tiles; fp32
                                        partial tiles in the split-K workspace (default
-                                       8192; 0 = never; at most 2^21) */
+                                       8192; 0 = never; at most 2^21); only while the
+                                       operator's estimated comp / comm ratio (the GEMM
+                                       at 1 PFLOP/s against the slower direction's
+                                       transfer) is below 2 */
 #define COMPASS_OPT_TAIL_MIN_K_128 14 /* the same for 128 x 128 tiles (default 0 = never) */
 #define COMPASS_OPT_TAIL_SLICE_K 15 /* least K depth of a tail slice, a positive multiple
                                        of 64 (default 2048) */

@@ -365,9 +365,9 @@ static int ensure_init() {
     return COMPASS_OK;
 }
 
-// Owning agent of a pointer (device memory -> GPU, host memory -> CPU).
-// The agent owning the allocation that holds `ptr`, and the end of that
-// allocation (*end, optional).
+// The agent owning the allocation that holds `ptr` (device memory -> the
+// GPU, host memory -> the CPU), and the end of that allocation (*end,
+// optional).
 static int agent_of(const void *ptr, hsa_agent_t *out, uintptr_t *end = nullptr) {
     Ctx &c = g_ctx;
     const uintptr_t u = (uintptr_t)ptr;
