@@ -178,6 +178,34 @@ def test_ag_gemm_tail_split_integer_exact(rank, ring):
     assert np.array_equal(host_bits(case.C), ref)
 
 
+def test_ag_gemm_tail_split_128_tiles_option_integer_exact():
+    # the tail split for 128 x 128 tiles (off by default): the fc1 shape, the
+    # last row-tile group (8 row tiles, the last ring step's two partitions)
+    # in 4 K slices of 1024, NaN-filled output
+    M, N, K, n = 8192, 2048, 4096, 8
+    inp = make_int_ag_inputs(M, N, K, n, seed=41)
+    ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
+    _say("ag tail split 128", M, N, K)
+    case = AGCase(inp, 2, "double")
+    case.C.fill_(0x7FC0)
+    try:
+        C.compass_set_option(C.OPT_TAIL_MIN_K_128, 4096)
+        C.compass_set_option(C.OPT_TAIL_SLICE_K, 1024)
+        C.compass_set_option(C.OPT_TAIL_GROUPS, 1)
+        C.compass_set_option(C.OPT_TILE_TRACE, 8192)
+        C.compass_ag_gemm(case.problem, C.links(200e9, 200e9))
+        C.compass_sync()
+        rec = C.compass_tile_trace(8192)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+        C.compass_set_option(C.OPT_TAIL_MIN_K_128, 0)
+        C.compass_set_option(C.OPT_TAIL_SLICE_K, 2048)
+        C.compass_set_option(C.OPT_TAIL_GROUPS, 2)
+    # 64 x 16 tiles of 128 x 128; the last group's 8 x 16 tiles in 4 slices
+    assert len(rec) == 64 * 16 + 8 * 16 * 3
+    assert np.array_equal(host_bits(case.C), ref)
+
+
 def test_ag_gemm_config1_all_ranks():
     # AllGather-GEMM, TP=2: shards 256x512 U[-1,1], B 512x1024, single ring
     inp = make_ag_inputs(512, 1024, 512, 2, seed=1, dist_a=("uniform", -1.0, 1.0), dist_w=("uniform", -1.0, 1.0))
