@@ -367,6 +367,15 @@ int compass_sync(void);
 #define COMPASS_OPT_TAIL_GROUPS  16 /* row-tile groups the tail split covers, 1..8
                                        (default 2); none when the launch has fewer than
                                        twice as many groups */
+#define COMPASS_OPT_HEAD_SPLIT  17 /* fused AllGather under the tail split's conditions
+                                       (256 x 256 tiles, K from COMPASS_OPT_TAIL_MIN_K,
+                                       estimated comp / comm ratio below 2): 1 = the tiles
+                                       of the leading row-tile groups whose partitions are
+                                       all resident (the rank's own chunk) split K into at
+                                       most 4 slices, as many as the workgroup slots over
+                                       their tiles, so that the work available before the
+                                       first remote partition lands occupies more CUs;
+                                       0 = off (default 1) */
 int compass_set_option(int key, long long value);
 
 /* Durations in microseconds of the GEMM kernels launched since the previous

@@ -45,6 +45,7 @@ OPT_TAIL_MIN_K = 13
 OPT_TAIL_MIN_K_128 = 14
 OPT_TAIL_SLICE_K = 15
 OPT_TAIL_GROUPS = 16
+OPT_HEAD_SPLIT = 17
 
 PATTERNS = {"ag": AG_GEMM, "rs": GEMM_RS}
 RING_DOUBLE_SPLIT = 2

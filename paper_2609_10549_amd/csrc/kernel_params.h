@@ -67,15 +67,20 @@ struct GemmParams {
     int spread_wait;
     uint32_t launch_seq;
     uint32_t *cu_slots;
-    // split K: work positions below split_from are whole tiles (tile
-    // position = work position); from split_from on, tile position
-    // t = split_from + u, slice j = work position split_from + u * ksplit + j,
-    // K range [j kslice, (j + 1) kslice). Every slice stores its fp32 partial
-    // tile at split_ws[(u * ksplit + j) * BM * BN]; the slice that counts
-    // split_cnt[u] up to ksplit sums the partials in slice order and runs the
-    // epilogue. ksplit == 1: no split (kslice = K); split_from == 0: every
-    // tile split.
+    // split K. Head: the first head_tiles tile positions split into
+    // head_split slices of head_kslice (work position u * head_split + j:
+    // tile u, slice j), workspace tiles [u * head_split, + head_split),
+    // counter u. Then whole tiles up to tile position split_from. From
+    // split_from on (the tail), tile position t = split_from + u, slice j,
+    // K range [j kslice, (j + 1) kslice), workspace tiles
+    // head_tiles * head_split + u * ksplit + j, counter head_tiles + u.
+    // Every slice stores its fp32 partial tile in the workspace; the slice
+    // that completes its tile's count sums the partials in slice order and
+    // runs the epilogue. ksplit == 1: no tail split (kslice = K);
+    // split_from == 0: every tile after the head split (needs head_tiles ==
+    // 0); head_tiles == 0: no head split.
     int ksplit, kslice, split_from;
+    int head_tiles, head_split, head_kslice;
     uint32_t *split_cnt;
     float *split_ws;
     // gating: flag index of partition p is flag_base + p. Arrival flags live
@@ -120,5 +125,12 @@ struct JoinParams {
     int count;
     uint16_t idx[kMaxJoin];
 };
+
+// Work items (tickets) of a launch: the head's slices, the whole tiles,
+// the tail's slices.
+__host__ __device__ inline int work_items(const GemmParams &p) {
+    const int tiles = p.tiles_m * p.tiles_n;
+    return p.head_tiles * p.head_split + (p.split_from - p.head_tiles) + (tiles - p.split_from) * p.ksplit;
+}
 
 }  // namespace compass

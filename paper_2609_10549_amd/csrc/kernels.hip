@@ -316,7 +316,8 @@ void gemm_kernel(const GemmParams p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm0 = (wave >> 1) * WM;
     const int wn0 = (wave & 1) * WN;
-    const int total = p.split_from + (p.tiles_m * p.tiles_n - p.split_from) * p.ksplit;
+    const int total = work_items(p);
+    const int head_items = p.head_tiles * p.head_split;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
 
@@ -350,13 +351,35 @@ void gemm_kernel(const GemmParams p) {
 
     while (pos < total) {
         // work position -> (tile position, K slice); `split`: this tile's K
-        // is split, its u-th split tile (u = tile position - split_from)
-        const bool split = p.ksplit > 1 && pos >= p.split_from;
-        const int u = split ? (pos - p.split_from) / p.ksplit : 0;
-        const int tpos = split ? p.split_from + u : pos;
-        const int slice = split ? pos - p.split_from - u * p.ksplit : 0;
-        const int kb = split ? slice * p.kslice : 0;
-        const int ke = split ? min(p.K, kb + p.kslice) : p.K;
+        // is split into `ns` slices, counted by split_cnt[uc], its partials
+        // at workspace tiles [wsf, wsf + ns)
+        bool split = false;
+        int tpos, slice = 0, ns = 1, uc = 0, wsf = 0, ksl = p.K;
+        if (pos < head_items) {
+            uc = pos / p.head_split;
+            slice = pos - uc * p.head_split;
+            tpos = uc;
+            split = true;
+            ns = p.head_split;
+            wsf = uc * p.head_split;
+            ksl = p.head_kslice;
+        } else {
+            const int q = pos - head_items + p.head_tiles;   // position in the unsplit-head order
+            if (p.ksplit > 1 && q >= p.split_from) {
+                const int u = (q - p.split_from) / p.ksplit;
+                slice = q - p.split_from - u * p.ksplit;
+                tpos = p.split_from + u;
+                split = true;
+                ns = p.ksplit;
+                uc = p.head_tiles + u;
+                wsf = head_items + u * p.ksplit;
+                ksl = p.kslice;
+            } else {
+                tpos = q;
+            }
+        }
+        const int kb = split ? slice * ksl : 0;
+        const int ke = split ? min(p.K, kb + ksl) : p.K;
         // tile position -> (row-tile ordinal, column tile): group_m rows at a time
         const int gsz = p.group_m * p.tiles_n;
         const int grp = tpos / gsz;
@@ -501,7 +524,7 @@ void gemm_kernel(const GemmParams p) {
         // slice order, so the result does not depend on which one was last
         bool finish = true;
         if (split) {
-            float *ws = p.split_ws + (size_t)(u * p.ksplit + slice) * (BM * BN);
+            float *ws = p.split_ws + (size_t)(wsf + slice) * (BM * BN);
             through_patch([&](int row, int col, f32x4 x) {
                 *reinterpret_cast<f32x4 *>(ws + row * BN + col) = x;
             });
@@ -512,10 +535,10 @@ void gemm_kernel(const GemmParams p) {
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             if (tid == 0) {
-                const uint32_t old = __hip_atomic_fetch_add(&p.split_cnt[u], 1u, __ATOMIC_RELAXED,
+                const uint32_t old = __hip_atomic_fetch_add(&p.split_cnt[uc], 1u, __ATOMIC_RELAXED,
                                                             __HIP_MEMORY_SCOPE_AGENT);
-                const bool last = old + 1u == (uint32_t)p.ksplit;
-                if (last) __hip_atomic_store(&p.split_cnt[u], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const bool last = old + 1u == (uint32_t)ns;
+                if (last) __hip_atomic_store(&p.split_cnt[uc], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 s_last = last;
             }
             __syncthreads();   // the partial loads below are issued after the count
@@ -535,7 +558,7 @@ void gemm_kernel(const GemmParams p) {
 
         if (finish) {
             if (split) {
-                const float *ws0 = p.split_ws + (size_t)u * p.ksplit * (BM * BN);
+                const float *ws0 = p.split_ws + (size_t)wsf * (BM * BN);
                 // B elements of 4 per thread at a time, all their slices' loads
                 // (and the partial sum's) in flight at once, then each summed in
                 // slice order: the workspace is uncached, so every load costs a
@@ -553,7 +576,7 @@ void gemm_kernel(const GemmParams p) {
                             const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
 #pragma unroll
                             for (int jj = 0; jj < S; ++jj)
-                                if (jj < p.ksplit)
+                                if (jj < ns)
                                     part[b][jj] = *reinterpret_cast<const f32x4 *>(ws0 + (size_t)jj * (BM * BN) +
                                                                                     row * BN + col);
                             pv[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -568,7 +591,7 @@ void gemm_kernel(const GemmParams p) {
                             f32x4 sum = part[b][0];
 #pragma unroll
                             for (int jj = 1; jj < S; ++jj)
-                                if (jj < p.ksplit) {
+                                if (jj < ns) {
                                     sum[0] += part[b][jj][0]; sum[1] += part[b][jj][1];
                                     sum[2] += part[b][jj][2]; sum[3] += part[b][jj][3];
                                 }
@@ -580,7 +603,7 @@ void gemm_kernel(const GemmParams p) {
                 // (half the batch in the ReduceScatter variant, whose partial-sum
                 // epilogue leaves fewer registers)
                 constexpr int BB = RS ? 2 : 4;
-                if (p.ksplit <= 8)
+                if (ns <= 8)
                     finish_split(std::integral_constant<int, BB>{}, std::integral_constant<int, 8>{});
                 else
                     finish_split(std::integral_constant<int, BB / 2>{}, std::integral_constant<int, kMaxSplit>{});

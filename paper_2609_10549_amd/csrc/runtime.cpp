@@ -87,7 +87,7 @@ constexpr int kSchedFineQueues = 1, kSchedSpread = 2, kSchedSplitK = 4;
 // split-K workspace: one fp32 partial tile per workgroup slot (the largest
 // of 256 x 256 on one workgroup per CU and 128 x 128 on two)
 constexpr int kMinSliceK = 512;      // K depth of a slice at least
-constexpr int kSplitWsTiles = 2;     // workspace: this many 256 x 256 fp32 partial tiles per CU
+constexpr int kSplitWsTiles = 3;     // workspace: this many 256 x 256 fp32 partial tiles per CU
 constexpr int kTailMinK = 8192;      // fused AllGather: split the tail's K from this depth on
 constexpr int kTailSliceK = 2048;    // ... into slices at least this deep, at most 4
 constexpr double kTailMaxLambda = 2.0;   // ... when the estimated comp / comm ratio is below this
@@ -180,6 +180,7 @@ struct Ctx {
     int tail_min_k[2] = {kTailMinK, 0};   // [0] 256 x 256, [1] 128 x 128
     int tail_slice_k = kTailSliceK;
     int tail_groups = 2;
+    bool head_split = true;               // fused AllGather: split the resident tiles' K (see set_head_split)
     // optional HIP events around every GEMM launch (kernel durations)
     bool timing = false;
     static constexpr int kTimed = 512;
@@ -1320,6 +1321,44 @@ static void set_tail_split(GemmParams &g, int cfg, double lam_est) {
     g.split_from = (groups - tail_groups) * g.group_m * g.tiles_n;
 }
 
+// Head split of a fused AllGather (the tail split's gates: 256 x 256 tiles
+// from K = kTailMinK, estimated lambda below kTailMaxLambda): until the
+// first remote partition lands only the resident partitions' tiles can run,
+// one per workgroup, and the other workgroups wait at their gates (GPT-3
+// AllGather, 4 : 1 ring: 96 tiles on 256 CUs for 65-135 us). The leading
+// row-tile groups of the ready order whose partitions are all resident
+// split K into s = min(4, slots / their tiles) slices, each at least
+// tail_slice_k deep, so that their work is spread over more workgroups and
+// done sooner; the workspace holds both the head's and the tail's partials.
+static void set_head_split(GemmParams &g, int cfg, double lam_est, uint64_t resident) {
+    Ctx &c = g_ctx;
+    const int min_k = c.tail_min_k[cfg == kTile256 ? 0 : 1];
+    if (!c.head_split || !(c.sched & kSchedSplitK) || !c.split_ws || min_k <= 0 || g.K < min_k) return;
+    if (!(lam_est < kTailMaxLambda) || !resident) return;
+    int rt = 0;   // leading row tiles of the ready order with every partition resident
+    while (rt < g.tiles_m) {
+        const int t = g.rt_order[rt];
+        const uint64_t lo = g.rt_lo[t], hi = g.rt_hi[t];
+        const uint64_t touch = (hi >= 63 ? ~0ull : ((2ull << hi) - 1ull)) & ~((1ull << lo) - 1ull);
+        if (touch & ~resident) break;
+        ++rt;
+    }
+    rt -= rt % g.group_m;   // positions walk whole row-tile groups
+    const int head = rt * g.tiles_n;
+    if (head == 0 || 2 * head > g.grid) return;
+    if (g.ksplit > 1 && g.split_from < head) return;
+    int sh = std::min(4, std::min(g.grid / head, g.K / c.tail_slice_k));
+    const size_t tile_bytes = (size_t)tile_rows(cfg) * tile_cols(cfg) * sizeof(float);
+    const int tiles = g.tiles_m * g.tiles_n;
+    const size_t tail_ws = g.ksplit > 1 ? (size_t)(tiles - g.split_from) * g.ksplit : 0;
+    const int tail_cnt = g.ksplit > 1 ? tiles - g.split_from : 0;
+    while (sh > 1 && ((size_t)head * sh + tail_ws) * tile_bytes > c.split_ws_bytes) --sh;
+    if (sh < 2 || head + tail_cnt > kMaxSplitTiles) return;
+    g.head_tiles = head;
+    g.head_split = sh;
+    g.head_kslice = ((g.K + sh - 1) / sh + 63) / 64 * 64;
+}
+
 static void touch_all(GemmParams &g, int nparts) {
     for (int t = 0; t < g.tiles_m; ++t) {
         g.rt_lo[t] = 0;
@@ -1721,7 +1760,7 @@ static int launch(const GemmParams &g0, int cfg, bool rs, hipStream_t s) {
         g.tile_trace = c.tile_trace;
         g.trace_base = c.trace_used;
         g.trace_cap = c.trace_cap;
-        const uint64_t work = (uint64_t)g0.split_from + ((uint64_t)g0.tiles_m * g0.tiles_n - g0.split_from) * g0.ksplit;
+        const uint64_t work = (uint64_t)work_items(g0);
         c.trace_used = std::min<uint64_t>(c.trace_cap, (uint64_t)c.trace_used + work);
     }
     const bool timed = c.timing && c.timed_count < Ctx::kTimed;
@@ -1850,6 +1889,7 @@ int op_ag_gemm(const compass_problem *p, const compass_links *l, void *stream) {
     if ((rc = expected_arrivals(p, geo, l, resident_mask(p, geo), arrive)) != COMPASS_OK) return rc;
     order_by_arrival(g, cfg, geo, p->M, true, arrive);
     set_tail_split(g, cfg, lam);
+    set_head_split(g, cfg, lam, resident_mask(p, geo));
     g.gate = kGateMain;
     g.nparts = geo.P;
     g.resident_mask = resident_mask(p, geo);
@@ -2167,6 +2207,10 @@ int op_set_option(int key, long long v) {
         if (v < 64 || v > (1 << 21) || v % 64) return set_error(COMPASS_ERR_INVALID, "tail slice depth must be a "
                                                                  "positive multiple of 64");
         c.tail_slice_k = (int)v;
+        return COMPASS_OK;
+    case COMPASS_OPT_HEAD_SPLIT:
+        if (v != 0 && v != 1) return set_error(COMPASS_ERR_INVALID, "head split option must be 0 or 1");
+        c.head_split = v == 1;
         return COMPASS_OK;
     case COMPASS_OPT_TAIL_GROUPS:
         if (v < 1 || v > 8) return set_error(COMPASS_ERR_INVALID, "tail groups must lie in [1, 8]");

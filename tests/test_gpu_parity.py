@@ -160,9 +160,11 @@ def test_ag_gemm_tail_split_integer_exact(rank, ring):
     # 32 x 17 tiles of 256 x 256; the last two row-tile groups (one
     # partition each) split K: double ring, 512-row partitions, 2 x 2 x 17
     # tiles in 4 slices; single ring, 1024-row partitions, 2 x 4 x 17 tiles
-    # in 3 slices (the 256 workgroups over a group's 68 tiles)
+    # in 3 slices (the 256 workgroups over a group's 68 tiles). The head:
+    # the rank's own chunk, 4 row tiles x 17 = 68 tiles, in 3 slices (the
+    # 256 workgroups over 68 tiles)
     extra = 68 * 3 if ring == "double" else 136 * 2
-    assert len(rec) == 32 * 17 + extra
+    assert len(rec) == 32 * 17 + extra + 68 * 2
     assert np.array_equal(host_bits(case.C), ref)
     # links unpaced (the engines' ceiling): the transfer is far shorter than
     # the GEMM (estimated comp / comm ratio above 2), so no tile splits
@@ -179,9 +181,9 @@ def test_ag_gemm_tail_split_integer_exact(rank, ring):
 
 
 def test_ag_gemm_tail_split_128_tiles_option_integer_exact():
-    # the tail split for 128 x 128 tiles (off by default): the fc1 shape, the
-    # last row-tile group (8 row tiles, the last ring step's two partitions)
-    # in 4 K slices of 1024, NaN-filled output
+    # the tail (and head) split for 128 x 128 tiles (off by default): the fc1
+    # shape, the last row-tile group (8 row tiles, the last ring step's two
+    # partitions) in 4 K slices of 1024, NaN-filled output
     M, N, K, n = 8192, 2048, 4096, 8
     inp = make_int_ag_inputs(M, N, K, n, seed=41)
     ref = O.f64_to_bf16_rne(O.ag_gemm([O.bf16_to_f64(s) for s in inp["shards"]], O.bf16_to_f64(inp["W"])))
@@ -201,8 +203,10 @@ def test_ag_gemm_tail_split_128_tiles_option_integer_exact():
         C.compass_set_option(C.OPT_TAIL_MIN_K_128, 0)
         C.compass_set_option(C.OPT_TAIL_SLICE_K, 2048)
         C.compass_set_option(C.OPT_TAIL_GROUPS, 2)
-    # 64 x 16 tiles of 128 x 128; the last group's 8 x 16 tiles in 4 slices
-    assert len(rec) == 64 * 16 + 8 * 16 * 3
+    # 64 x 16 tiles of 128 x 128; the last group's 8 x 16 tiles in 4 slices,
+    # and (the head split, under the same depth gate) the rank's own chunk,
+    # one group of 8 x 16 tiles, in 4 slices too
+    assert len(rec) == 64 * 16 + 8 * 16 * 3 + 8 * 16 * 3
     assert np.array_equal(host_bits(case.C), ref)
 
 
