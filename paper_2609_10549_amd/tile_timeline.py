@@ -26,7 +26,14 @@ tail after the last arrival, and the work items' time split into waiting at
 the gate, main loop and epilogue. AllGather tiles wait before their main
 loop (for the rows they read); ReduceScatter tiles wait in the epilogue (for
 the incoming partial of their rows), and for them the send start of each
-partition (when the copy side saw its last tile done) is reported too."""
+partition (when the copy side saw its last tile done) is reported too.
+
+Occupancy: the launch's workgroup slots (the most items ever in flight at
+once, from ticket to epilogue end) against time, in bins: per bin the mean
+number of items in flight and how many of them wait at the gate, run the
+main loop or the epilogue, and the idle slot time before and after the last
+arrival flag (a slot is idle between the end of one item and the next
+ticket, and after its last item until the launch's end)."""
 from __future__ import annotations
 
 import argparse
@@ -73,8 +80,47 @@ def child(name: str, rates, tiles_npy: str, opts=(), slice_bytes: int = 0) -> No
     C.compass_set_option(C.OPT_TILE_TRACE, 0)
 
 
+def occupancy(tick, gate, loop, end, pattern: str, bin_us: float, t_split_us: float) -> dict:
+    """Items in flight per time bin (microseconds from the first ticket) and
+    the idle slot time before and after `t_split_us`; tick..end in 100 MHz
+    counter ticks."""
+    t0 = tick.min()
+    t = lambda x: (x.astype(np.float64) - t0) / 100.0  # noqa: E731
+    a, e = t(tick), t(end)
+    if pattern == "ag":
+        phases = [("wait", a, t(gate)), ("main", t(gate), t(loop)), ("epilogue", t(loop), e)]
+    else:
+        phases = [("main", a, t(loop)), ("wait", t(loop), t(gate)), ("epilogue", t(gate), e)]
+    ev = np.concatenate([np.stack([a, np.ones_like(a)], 1), np.stack([e, -np.ones_like(e)], 1)])
+    ev = ev[np.lexsort((ev[:, 1], ev[:, 0]))]     # ends before starts at equal times
+    slots = int(np.cumsum(ev[:, 1]).max())
+    span = float(e.max())
+
+    def overlap(lo, hi, b0, b1):
+        return np.clip(np.minimum(hi, b1) - np.maximum(lo, b0), 0.0, None).sum()
+
+    bins = []
+    edges = np.arange(0.0, span + bin_us, bin_us)
+    for b0 in edges[:-1].tolist():
+        b1 = min(b0 + bin_us, span)
+        w = b1 - b0
+        if w <= 0:
+            continue
+        row = {"from_us": round(float(b0), 1), "in_flight": round(float(overlap(a, e, b0, b1)) / w, 1)}
+        for name, lo, hi in phases:
+            row[name] = round(float(overlap(lo, hi, b0, b1)) / w, 1)
+        bins.append(row)
+    busy_before = float(overlap(a, e, 0.0, t_split_us))
+    busy_after = float(overlap(a, e, t_split_us, span))
+    before, after = slots * min(t_split_us, span), slots * max(span - t_split_us, 0.0)
+    return {"slots": slots, "bin_us": bin_us, "bins": bins,
+            "busy_share": round(float((e - a).sum()) / (slots * span), 3),
+            "idle_slot_us_before_last_flag": round(before - busy_before, 1),
+            "idle_slot_us_after_last_flag": round(after - busy_after, 1)}
+
+
 def analyse(copy_csv: str, tiles: np.ndarray, pattern: str, M: int, n: int, ring: str,
-            tile_rows: int | None = None) -> dict:
+            tile_rows: int | None = None, bin_us: float = 50.0) -> dict:
     """Per-partition and whole-launch figures (microseconds from the first
     ticket) of the traced (last) call in `copy_csv` and its tile records."""
     rows_ = list(csv.DictReader(open(copy_csv)))
@@ -112,7 +158,8 @@ def analyse(copy_csv: str, tiles: np.ndarray, pattern: str, M: int, n: int, ring
            "last_flag_us": round(last_flag, 1), "tail_after_last_flag_us": round(span - last_flag, 1),
            "share_wait": round(float(wait.sum()) / tot, 3), "share_main": round(float(main.sum()) / tot, 3),
            "share_epilogue": round(float(epi.sum()) / tot, 3),
-           "mean_main_us": round(float(main.mean()), 1), "partitions": per}
+           "mean_main_us": round(float(main.mean()), 1), "partitions": per,
+           "occupancy": occupancy(tick, gate, loop, end, pattern, bin_us, last_flag)}
     # the tiles of the last-arriving partitions (the last ring step)
     if flags:
         last = sorted(flags, key=flags.get)[-(2 if ring.startswith("double") else 1):]
@@ -145,6 +192,12 @@ def markdown(name: str, res: dict, command: str) -> str:
         L.append(f"* last ring step (partitions {s['partitions']}, flags at {s['flags_us']} µs): {s['items']} items, "
                  f"gates passed {s['first_gate_us']}–{s['last_gate_us']} µs, main loop mean {s['mean_main_us']} / "
                  f"max {s['max_main_us']} µs, epilogue mean {s['mean_epilogue_us']} µs, last end {s['last_end_us']} µs")
+    oc = res["occupancy"]
+    L.append(f"* occupancy: {oc['slots']} workgroup slots busy {100 * oc['busy_share']:.1f} % of the span; idle slot "
+             f"time {oc['idle_slot_us_before_last_flag']} µs before the last flag, "
+             f"{oc['idle_slot_us_after_last_flag']} µs after it (÷ {oc['slots']}: "
+             f"{oc['idle_slot_us_before_last_flag'] / oc['slots']:.1f} / "
+             f"{oc['idle_slot_us_after_last_flag'] / oc['slots']:.1f} µs of the whole launch)")
     L += ["", "| partition | items | flag | first gate | last end | wait | main loop | epilogue |"
           + (" send start |" if pat == "rs" else ""),
           "|---|---|---|---|---|---|---|---|" + ("---|" if pat == "rs" else "")]
@@ -152,6 +205,10 @@ def markdown(name: str, res: dict, command: str) -> str:
         L.append(f"| {p['partition']} | {p['items']} | {p['flag_us']} | {p['first_gate_us']} | {p['last_end_us']} | "
                  f"{p['wait_us']} | {p['main_us']} | {p['epilogue_us']} |"
                  + (f" {p['send_start_us']} |" if pat == "rs" else ""))
+    L += ["", f"Items in flight per {oc['bin_us']:g} µs bin (mean over the bin):", "",
+          "| from µs | in flight | waiting | main loop | epilogue |", "|---|---|---|---|---|"]
+    for b in oc["bins"]:
+        L.append(f"| {b['from_us']} | {b['in_flight']} | {b['wait']} | {b['main']} | {b['epilogue']} |")
     return "\n".join(L) + "\n"
 
 

@@ -191,6 +191,14 @@ def test_tile_timeline_splits_item_time(tmp_path):
     tot = 11 + 11 + 45 + 60
     assert abs(r["share_wait"] - round((30 + 48) / tot, 3)) < 1e-9
     assert r["last_step"]["partitions"] == [2, 3] and r["last_step"]["last_end_us"] == 62.0
+    # occupancy: at most 4 items in flight (all four start by 12 us), busy
+    # 11 + 11 + 45 + 60 of 4 x 62 slot-us; idle slot time before the last
+    # flag (50 us): 39 + 39 + 5 + 2 (the last item's ticket at 2 us)
+    oc = r["occupancy"]
+    assert oc["slots"] == 4 and abs(oc["busy_share"] - round(127 / 248, 3)) < 1e-9
+    assert oc["idle_slot_us_before_last_flag"] == 85.0 and oc["idle_slot_us_after_last_flag"] == 36.0
+    b0 = oc["bins"][0]   # 0..50 us: 4 items in flight 11, 11, 45, 48 us
+    assert b0["in_flight"] == round(115 / 50, 1) and b0["wait"] == round(78 / 50, 1)
     # ReduceScatter: the gate is the epilogue's, after the main loop
     t = np.array([rec(2, 1000, 5000, 3000, 5200)], dtype=np.uint32)
     r = TT.analyse(str(path), t, "rs", 64, 2, "double", tile_rows=16)
