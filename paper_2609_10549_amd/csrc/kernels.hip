@@ -562,9 +562,13 @@ void gemm_kernel(const GemmParams p) {
                 // B elements of 4 per thread at a time, all their slices' loads
                 // (and the partial sum's) in flight at once, then each summed in
                 // slice order: the workspace is uncached, so every load costs a
-                // memory round trip, and B of them overlap
-                auto finish_split = [&](auto b_const, auto s_const) {
+                // memory round trip, and B x S of them overlap. With the slice
+                // count a compile-time constant (EX) the loads carry no branch,
+                // and the waits before the sums count them exactly; otherwise
+                // S is an upper bound and slices from ns on are skipped.
+                auto finish_split = [&](auto b_const, auto s_const, auto ex_const) {
                     constexpr int B = decltype(b_const)::value, S = decltype(s_const)::value;
+                    constexpr bool EX = decltype(ex_const)::value;
                     constexpr int E = BM * BN / 4;
                     static_assert(E % (kThreads * B) == 0, "whole batches");
                     for (int e0 = tid; e0 < E; e0 += kThreads * B) {
@@ -576,7 +580,7 @@ void gemm_kernel(const GemmParams p) {
                             const int row = e / (BN / 4), col = (e - row * (BN / 4)) * 4;
 #pragma unroll
                             for (int jj = 0; jj < S; ++jj)
-                                if (jj < ns)
+                                if (EX || jj < ns)
                                     part[b][jj] = *reinterpret_cast<const f32x4 *>(ws0 + (size_t)jj * (BM * BN) +
                                                                                     row * BN + col);
                             pv[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -591,7 +595,7 @@ void gemm_kernel(const GemmParams p) {
                             f32x4 sum = part[b][0];
 #pragma unroll
                             for (int jj = 1; jj < S; ++jj)
-                                if (jj < ns) {
+                                if (EX || jj < ns) {
                                     sum[0] += part[b][jj][0]; sum[1] += part[b][jj][1];
                                     sum[2] += part[b][jj][2]; sum[3] += part[b][jj][3];
                                 }
@@ -600,13 +604,27 @@ void gemm_kernel(const GemmParams p) {
                         }
                     }
                 };
-                // (half the batch in the ReduceScatter variant, whose partial-sum
-                // epilogue leaves fewer registers)
-                constexpr int BB = RS ? 2 : 4;
-                if (ns <= 8)
-                    finish_split(std::integral_constant<int, BB>{}, std::integral_constant<int, 8>{});
-                else
-                    finish_split(std::integral_constant<int, BB / 2>{}, std::integral_constant<int, kMaxSplit>{});
+                // The host splits a tile into 2 to 8 slices (more only through
+                // kMaxSplit): each count has its own branch-free instance. Batches
+                // of 4 elements (2 from 5 slices on, and in the ReduceScatter
+                // variant, whose partial-sum epilogue leaves fewer registers) keep
+                // the loads within the registers the main loop leaves, with no
+                // spills.
+                constexpr int BL = RS ? 2 : 4;
+                using yes = std::true_type;
+                using no = std::false_type;
+                using std::integral_constant;
+                switch (ns) {
+                case 2: finish_split(integral_constant<int, BL>{}, integral_constant<int, 2>{}, yes{}); break;
+                case 3: finish_split(integral_constant<int, BL>{}, integral_constant<int, 3>{}, yes{}); break;
+                case 4: finish_split(integral_constant<int, BL>{}, integral_constant<int, 4>{}, yes{}); break;
+                case 5: finish_split(integral_constant<int, 2>{}, integral_constant<int, 5>{}, yes{}); break;
+                case 6: finish_split(integral_constant<int, 2>{}, integral_constant<int, 6>{}, yes{}); break;
+                case 7: finish_split(integral_constant<int, 2>{}, integral_constant<int, 7>{}, yes{}); break;
+                case 8: finish_split(integral_constant<int, 2>{}, integral_constant<int, 8>{}, yes{}); break;
+                default:
+                    finish_split(integral_constant<int, BL / 2>{}, integral_constant<int, kMaxSplit>{}, no{});
+                }
             } else if (has_p) {
                 // as through_patch, with each 32 x 32 block's fp32 partial
                 // brought into LDS by buffer_load ... lds two blocks ahead of

@@ -33,7 +33,8 @@ once, from ticket to epilogue end) against time, in bins: per bin the mean
 number of items in flight and how many of them wait at the gate, run the
 main loop or the epilogue, and the idle slot time before and after the last
 arrival flag (a slot is idle between the end of one item and the next
-ticket, and after its last item until the launch's end)."""
+ticket, and after its last item until the launch's end), and per XCD (the
+record's XCC_ID) its items and when its last item ended."""
 from __future__ import annotations
 
 import argparse
@@ -80,7 +81,7 @@ def child(name: str, rates, tiles_npy: str, opts=(), slice_bytes: int = 0) -> No
     C.compass_set_option(C.OPT_TILE_TRACE, 0)
 
 
-def occupancy(tick, gate, loop, end, pattern: str, bin_us: float, t_split_us: float) -> dict:
+def occupancy(tick, gate, loop, end, pattern: str, bin_us: float, t_split_us: float, xcc=None) -> dict:
     """Items in flight per time bin (microseconds from the first ticket) and
     the idle slot time before and after `t_split_us`; tick..end in 100 MHz
     counter ticks."""
@@ -113,7 +114,13 @@ def occupancy(tick, gate, loop, end, pattern: str, bin_us: float, t_split_us: fl
     busy_before = float(overlap(a, e, 0.0, t_split_us))
     busy_after = float(overlap(a, e, t_split_us, span))
     before, after = slots * min(t_split_us, span), slots * max(span - t_split_us, 0.0)
-    return {"slots": slots, "bin_us": bin_us, "bins": bins,
+    per_xcd = []
+    if xcc is not None:
+        for x in sorted(set(xcc.tolist())):
+            m = xcc == x
+            per_xcd.append({"xcd": int(x), "items": int(m.sum()), "last_end_us": round(float(e[m].max()), 1),
+                            "busy_us": round(float((e[m] - a[m]).sum()), 1)})
+    return {"slots": slots, "bin_us": bin_us, "bins": bins, "per_xcd": per_xcd,
             "busy_share": round(float((e - a).sum()) / (slots * span), 3),
             "idle_slot_us_before_last_flag": round(before - busy_before, 1),
             "idle_slot_us_after_last_flag": round(after - busy_after, 1)}
@@ -159,7 +166,7 @@ def analyse(copy_csv: str, tiles: np.ndarray, pattern: str, M: int, n: int, ring
            "share_wait": round(float(wait.sum()) / tot, 3), "share_main": round(float(main.sum()) / tot, 3),
            "share_epilogue": round(float(epi.sum()) / tot, 3),
            "mean_main_us": round(float(main.mean()), 1), "partitions": per,
-           "occupancy": occupancy(tick, gate, loop, end, pattern, bin_us, last_flag)}
+           "occupancy": occupancy(tick, gate, loop, end, pattern, bin_us, last_flag, rec[:, 3])}
     # the tiles of the last-arriving partitions (the last ring step)
     if flags:
         last = sorted(flags, key=flags.get)[-(2 if ring.startswith("double") else 1):]
@@ -198,6 +205,9 @@ def markdown(name: str, res: dict, command: str) -> str:
              f"{oc['idle_slot_us_after_last_flag']} µs after it (÷ {oc['slots']}: "
              f"{oc['idle_slot_us_before_last_flag'] / oc['slots']:.1f} / "
              f"{oc['idle_slot_us_after_last_flag'] / oc['slots']:.1f} µs of the whole launch)")
+    if oc["per_xcd"]:
+        L.append("* per XCD (items, busy µs, last end µs): " + "; ".join(
+            f"{x['xcd']}: {x['items']}, {x['busy_us']:.0f}, {x['last_end_us']}" for x in oc["per_xcd"]))
     L += ["", "| partition | items | flag | first gate | last end | wait | main loop | epilogue |"
           + (" send start |" if pat == "rs" else ""),
           "|---|---|---|---|---|---|---|---|" + ("---|" if pat == "rs" else "")]
@@ -220,6 +230,7 @@ def main():
                     help="library option NAME=VALUE (NAME as in OPT_NAME of the binding), repeatable")
     ap.add_argument("--slice-bytes", type=int, default=0, help="largest single copy (links.slice_bytes; 0: default)")
     ap.add_argument("--out", default=None, help="markdown summary file")
+    ap.add_argument("--keep", default=None, help="directory to keep the raw copy-side and tile traces in")
     ap.add_argument("--child", default=None, help=argparse.SUPPRESS)
     args = ap.parse_args()
     pat, M, N, K, n, ring, rates = WORKLOADS[args.workload]
@@ -244,9 +255,14 @@ def main():
         if rc != 0:
             raise SystemExit(f"child failed with status {rc}")
         res = analyse(trace_csv, np.load(tiles_npy), pat, M, n, ring)
+        if args.keep:
+            import shutil
+            os.makedirs(args.keep, exist_ok=True)
+            shutil.copy(trace_csv, os.path.join(args.keep, f"{args.workload}_copy.csv"))
+            shutil.copy(tiles_npy, os.path.join(args.keep, f"{args.workload}_tiles.npy"))
     res["rates"] = "unpaced" if not rates else f"{rates[0] / 1e9:g} / {rates[1] / 1e9:g} GB/s"
     command = "python -m paper_2609_10549_amd.tile_timeline " + " ".join(
-        a for a in sys.argv[1:] if not a.startswith("--out") and a != args.out)
+        a for a in sys.argv[1:] if not a.startswith(("--out", "--keep")) and a not in (args.out, args.keep))
     text = markdown(args.workload, res, command.strip())
     print(text, flush=True)
     if args.out:
