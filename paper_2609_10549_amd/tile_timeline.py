@@ -19,6 +19,11 @@ kernel's first workgroup start) as the first ticket. That puts a host event
 at most the start word's one-way delay (about a microsecond, measured by
 flag_latency) too early.
 
+Before the traced call, five untraced ones are timed by HIP events around
+the GEMM launch and by the host clock from the call to its synchronised end
+(the operator's whole cost: staging, copy-side submission, kernel, join); the
+launch span below runs from the first ticket to the last epilogue end.
+
 Reported per partition (the row range one arrival flag covers): its flag
 time, its tiles' first gate pass and last epilogue end, and the mean wait,
 main-loop and epilogue time of its tiles; then the whole launch's span, the
@@ -39,6 +44,7 @@ from __future__ import annotations
 
 import argparse
 import csv
+import json
 import os
 import subprocess
 import sys
@@ -74,11 +80,27 @@ def child(name: str, rates, tiles_npy: str, opts=(), slice_bytes: int = 0) -> No
     while time.perf_counter() - t0 < 0.25:
         op(buf.problem, lk)
         C.compass_sync()
+    # five untraced calls, timed by the host clock (call to synchronised
+    # end) and by HIP events around the GEMM launch, then the traced one
+    C.compass_set_option(C.OPT_KERNEL_TIMING, 1)
+    C.compass_kernel_times()
+    wall = []
+    for _ in range(5):
+        t1 = time.perf_counter()
+        op(buf.problem, lk)
+        C.compass_sync()
+        wall.append((time.perf_counter() - t1) * 1e6)
+    kern = C.compass_kernel_times()
     C.compass_set_option(C.OPT_TILE_TRACE, TRACE_CAP)
     op(buf.problem, lk)
     C.compass_sync()
+    kern_traced = C.compass_kernel_times()
+    C.compass_set_option(C.OPT_KERNEL_TIMING, 0)
     np.save(tiles_npy, C.compass_tile_trace(TRACE_CAP))
     C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    with open(tiles_npy + ".json", "w") as f:
+        json.dump({"op_wall_us": float(np.median(wall)), "kernel_event_us": float(np.median(kern)),
+                   "kernel_event_us_traced": float(kern_traced[-1])}, f)
 
 
 def occupancy(tick, gate, loop, end, pattern: str, bin_us: float, t_split_us: float, xcc=None) -> dict:
@@ -190,7 +212,11 @@ def markdown(name: str, res: dict, command: str) -> str:
          f"Command: `{command}`", "",
          f"Rates (fast / slow direction): {res.get('rates', 'unpaced')}. Times in µs from the launch's first "
          "ticket; host events placed by the copy side's start-seen time (≤ ~1 µs early).", "",
-         f"* work items: {res['items']} ({res['tile_rows']}-row tiles), launch span {res['span_us']} µs",
+         f"* work items: {res['items']} ({res['tile_rows']}-row tiles), launch span {res['span_us']} µs"
+         + (f" (first ticket to last epilogue end; the traced launch by HIP events "
+            f"{res['times']['kernel_event_us_traced']} µs; five untraced calls, median: launch "
+            f"{res['times']['kernel_event_us']} µs by HIP events, {res['times']['op_wall_us']} µs from the call to "
+            f"its synchronised end)" if "times" in res else ""),
          f"* last arrival flag at {res['last_flag_us']} µs; tail after it {res['tail_after_last_flag_us']} µs",
          f"* work-item time: {100 * res['share_wait']:.1f} % waiting at the gate, {100 * res['share_main']:.1f} % "
          f"main loop, {100 * res['share_epilogue']:.1f} % epilogue (mean main loop {res['mean_main_us']} µs)"]
@@ -255,11 +281,14 @@ def main():
         if rc != 0:
             raise SystemExit(f"child failed with status {rc}")
         res = analyse(trace_csv, np.load(tiles_npy), pat, M, n, ring)
+        with open(tiles_npy + ".json") as f:
+            res["times"] = {k: round(v, 1) for k, v in json.load(f).items()}
         if args.keep:
             import shutil
             os.makedirs(args.keep, exist_ok=True)
             shutil.copy(trace_csv, os.path.join(args.keep, f"{args.workload}_copy.csv"))
             shutil.copy(tiles_npy, os.path.join(args.keep, f"{args.workload}_tiles.npy"))
+            shutil.copy(tiles_npy + ".json", os.path.join(args.keep, f"{args.workload}_times.json"))
     res["rates"] = "unpaced" if not rates else f"{rates[0] / 1e9:g} / {rates[1] / 1e9:g} GB/s"
     command = "python -m paper_2609_10549_amd.tile_timeline " + " ".join(
         a for a in sys.argv[1:] if not a.startswith(("--out", "--keep")) and a not in (args.out, args.keep))
