@@ -205,9 +205,13 @@ int compass_partition_layout(int pattern, int ring, int n, int rank, int M, cons
  *   partial_src[c], c = 0..n-1: (M/n) x N fp32 incoming partial sum of row
  *     chunk c (device or pinned host). The partial of the rank's first
  *     ReduceScatter step (a true ring has none there) is treated as resident:
- *     unless partial_src of that chunk already points at its rows of
- *     partial_stage, it is copied there (on the stream) before the operator
- *     starts. The other n-1 arrive over the emulated link in ring order.
+ *     in device memory, with the resident rows on tile boundaries (the usual
+ *     case), the GEMM's epilogue reads it from partial_src directly (d = 1,
+ *     fused and sequential); otherwise, unless partial_src of that chunk
+ *     already points at its rows of partial_stage, it is copied there (on
+ *     the stream) before the operator starts; either way the caller keeps it
+ *     unchanged until the call's work on the stream is done. The other n-1
+ *     arrive over the emulated link in ring order.
  *   partial_stage: device, M x N fp32 landing buffer (chunk c at its rows).
  *   C: device, M x N bf16: row chunk c = bf16(A[chunk c] * W^T + partial c).
  *   send_dst: NULL, or n pointers; for every chunk c != rank, send_dst[c]

@@ -40,6 +40,11 @@ struct GemmParams {
     const uint16_t *W;   // bf16, N x K
     uint16_t *C;         // bf16 output, rows addressed through the row map
     const float *P;      // fp32 partial added before rounding (or null)
+    // aliased partial rows: the partial of (mapped) rows [palt_lo[i],
+    // palt_hi[i]) is read from palt[i] + (row - palt_lo[i]) * ldp instead of
+    // P (each range a whole number of tiles; empty when lo == hi)
+    const float *palt[2];
+    int palt_lo[2], palt_hi[2];
     // extents in bytes; a tile's buffer loads (and, with a partial, its
     // stores of C) are bounded by them, from a base at the tile's first row
     // of A, P and C (its first column of W), with 32-bit offsets from there

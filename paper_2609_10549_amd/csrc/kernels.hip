@@ -495,6 +495,21 @@ void gemm_kernel(const GemmParams p) {
             }
         };
         const int mlim = failed ? 0 : p.M;   // a failed tile stores nothing
+        // the tile's partial sum: from P, or, for the rows of an aliased
+        // range (a whole number of tiles), from that range's own buffer
+        const float *pbase = p.P;
+        int plo = 0;
+        uint64_t pbytes = p.p_bytes;
+        if (RS) {
+            const int pm0 = map_row(p, m0);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                if (pm0 >= p.palt_lo[i] && pm0 < p.palt_hi[i]) {
+                    pbase = p.palt[i];
+                    plo = p.palt_lo[i];
+                    pbytes = (uint64_t)(p.palt_hi[i] - plo) * (uint64_t)p.ldp * 4u;
+                }
+        }
         // a tile of a chunk that is sent on (ReduceScatter) stores with
         // system-scope write-through, so that no L2 write-back is needed
         // before the copy engines read it
@@ -506,7 +521,7 @@ void gemm_kernel(const GemmParams p) {
             if (m < mlim && n < p.N) {
                 const int pm = map_row(p, m);
                 if (add_p) {
-                    const f32x4 pv = *reinterpret_cast<const f32x4 *>(p.P + (size_t)pm * p.ldp + n);
+                    const f32x4 pv = *reinterpret_cast<const f32x4 *>(pbase + (size_t)(pm - plo) * p.ldp + n);
                     v0 += pv[0]; v1 += pv[1]; v2 += pv[2]; v3 += pv[3];
                 }
                 const uint64_t o = (uint64_t)pack_bf16x2(v0, v1) | ((uint64_t)pack_bf16x2(v2, v3) << 32);
@@ -586,7 +601,8 @@ void gemm_kernel(const GemmParams p) {
                             pv[b] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
                             const int m = m0 + row, n = n0 + col;
                             if (has_p && m < p.M && n < p.N)
-                                pv[b] = *reinterpret_cast<const f32x4 *>(p.P + (size_t)map_row(p, m) * p.ldp + n);
+                                pv[b] = *reinterpret_cast<const f32x4 *>(pbase + (size_t)(map_row(p, m) - plo) * p.ldp +
+                                                                         n);
                         }
 #pragma unroll
                         for (int b = 0; b < B; ++b) {
@@ -642,7 +658,7 @@ void gemm_kernel(const GemmParams p) {
                 constexpr int NSLOT = 3, AHEAD = NSLOT - 1;
                 const int prow0 = map_row(p, m0);
                 const __amdgpu_buffer_rsrc_t rP =
-                    tile_rsrc(p.P, p.p_bytes, (uint64_t)prow0 * (uint64_t)p.ldp * 4u);
+                    tile_rsrc(pbase, pbytes, (uint64_t)(prow0 - plo) * (uint64_t)p.ldp * 4u);
                 const int rr = lane >> 3, rc = lane & 7;
                 char *const pslot[NSLOT] = {sA1 + wave * 4096, sW0 + wave * 4096, sW1 + wave * 4096};
                 const __amdgpu_buffer_rsrc_t rC =

@@ -1729,6 +1729,51 @@ static int stage_local_shard(const compass_problem *p, const Geometry &geo, hipS
     return e == hipSuccess ? COMPASS_OK : hip_fail(e, "local shard copy");
 }
 
+// The first step's partials (the resident partitions) read by the kernel
+// straight from the caller's buffers, with no staging copy: per chunk, the
+// rows its resident partitions cover, contiguous in the chunk, become an
+// aliased row range of the landing buffer (GemmParams::palt) whose partial
+// the epilogue reads from partial_src[c]. Needs device memory, the identity
+// row map, range ends on tile boundaries (no tile reads two buffers) and at
+// most two ranges; *aliased false otherwise, and the caller stages them.
+static int alias_resident_partials(GemmParams &g, const compass_problem *p, const Geometry &geo, uint64_t resident,
+                                   int cfg, bool *aliased) {
+    *aliased = false;
+    if (g.piece != 0) return COMPASS_OK;
+    const int bm = tile_rows(cfg);
+    int lo[2], hi[2], chunk[2], k = 0;
+    for (int c = 0; c < p->n; ++c) {
+        int a = geo.rows, b = -1, rows = 0;
+        for (int q = 0; q < geo.P; ++q) {
+            if (!((resident >> q) & 1ull) || part_chunk(geo, q) != c) continue;
+            int off, cnt;
+            part_rows(geo, geo.rows, q, &off, &cnt);
+            a = std::min(a, off);
+            b = std::max(b, off + cnt);
+            rows += cnt;
+        }
+        if (b < 0) continue;
+        const int plo = c * geo.rows + a, phi = c * geo.rows + b;
+        if (k == 2 || rows != b - a || plo % bm || (phi % bm && phi != p->M)) return COMPASS_OK;
+        hsa_agent_t owner;
+        const int rc = agent_of(p->partial_src[c], &owner);
+        if (rc != COMPASS_OK) return rc;
+        if (owner.handle != g_ctx.gpu.handle) return COMPASS_OK;
+        lo[k] = plo;
+        hi[k] = phi;
+        chunk[k] = c;
+        ++k;
+    }
+    for (int i = 0; i < k; ++i) {
+        g.palt[i] = (const float *)((const char *)p->partial_src[chunk[i]] + (size_t)(lo[i] - chunk[i] * geo.rows) *
+                                                                               (size_t)p->N * 4);
+        g.palt_lo[i] = lo[i];
+        g.palt_hi[i] = hi[i];
+    }
+    *aliased = true;
+    return COMPASS_OK;
+}
+
 // The partials of the resident partitions, for each of the d sub-operators
 // the rows its piece of the partition covers (rs_jobs moves the others).
 static int stage_resident_partials(const compass_problem *p, const Geometry &geo, uint64_t resident, int d,
@@ -1909,11 +1954,13 @@ int op_gemm_rs(const compass_problem *p, const compass_links *l, void *stream) {
     const uint64_t res = resident_mask(p, geo);
     Job jobs[4];
     if ((rc = rs_jobs(p, geo, l, epoch, 1, res, true, true, jobs)) != COMPASS_OK) return rc;
-    if ((rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
     const int cfg = pick_tile(p->M, p->N, true, min_part_rows(geo), lambda_estimate(p, geo, l), true);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
+    bool aliased = false;
+    if ((rc = alias_resident_partials(g, p, geo, res, cfg, &aliased)) != COMPASS_OK) return rc;
+    if (!aliased && (rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     // ReduceScatter tiles compute before their partial is needed, so they
     // run in ring-step order (a step's partitions on both rings together),
     // not in arrival order: under a 4 : 1 ring the faster ring's partials
@@ -2088,11 +2135,13 @@ int op_sequential(const compass_problem *p, const compass_links *l, void *stream
     const uint64_t res = resident_mask(p, geo);
     Job jobs[4];
     if ((rc = rs_jobs(p, geo, l, epoch, 1, res, false, true, jobs)) != COMPASS_OK) return rc;
-    if ((rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     GemmParams g;
     init_params(g, epoch);
     const int cfg = pick_tile(p->M, p->N, false);
     if ((rc = set_shape(g, cfg, p->M, p->N, p->K, p->A, p->M, p->W, p->C, p->partial_stage)) != COMPASS_OK) return rc;
+    bool aliased = false;
+    if ((rc = alias_resident_partials(g, p, geo, res, cfg, &aliased)) != COMPASS_OK) return rc;
+    if (!aliased && (rc = stage_resident_partials(p, geo, res, 1, s)) != COMPASS_OK) return rc;
     g.gate = kGateNone;
     set_split(g, cfg);
     if ((rc = launch(g, cfg, true, s)) != COMPASS_OK) return rc;
