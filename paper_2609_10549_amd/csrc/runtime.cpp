@@ -1733,9 +1733,10 @@ static int stage_local_shard(const compass_problem *p, const Geometry &geo, hipS
 // straight from the caller's buffers, with no staging copy: per chunk, the
 // rows its resident partitions cover, contiguous in the chunk, become an
 // aliased row range of the landing buffer (GemmParams::palt) whose partial
-// the epilogue reads from partial_src[c]. Needs device memory, the identity
-// row map, range ends on tile boundaries (no tile reads two buffers) and at
-// most two ranges; *aliased false otherwise, and the caller stages them.
+// the epilogue reads from partial_src[c]. Needs device memory 16-byte
+// aligned, the identity row map, range ends on tile boundaries (no tile
+// reads two buffers) and at most two ranges; *aliased false otherwise, and
+// the caller stages them.
 static int alias_resident_partials(GemmParams &g, const compass_problem *p, const Geometry &geo, uint64_t resident,
                                    int cfg, bool *aliased) {
     *aliased = false;
@@ -1755,6 +1756,8 @@ static int alias_resident_partials(GemmParams &g, const compass_problem *p, cons
         if (b < 0) continue;
         const int plo = c * geo.rows + a, phi = c * geo.rows + b;
         if (k == 2 || rows != b - a || plo % bm || (phi % bm && phi != p->M)) return COMPASS_OK;
+        // (the epilogue reads the partial 16 bytes at a time)
+        if ((uintptr_t)p->partial_src[c] % 16) return COMPASS_OK;
         hsa_agent_t owner;
         const int rc = agent_of(p->partial_src[c], &owner);
         if (rc != COMPASS_OK) return rc;
