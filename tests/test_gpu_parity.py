@@ -278,6 +278,41 @@ def test_gemm_rs_integer_exact(ring, n):
                 assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
 
 
+@pytest.mark.parametrize("ring,source", [("single", "device"), ("double", "device"), ("single", "misaligned"),
+                                         ("double", "misaligned"), ("single", "pinned")])
+def test_gemm_rs_first_step_partial_sources_integer_exact(ring, source):
+    # the first ring step's partials (resident from the start): read in place
+    # from device memory (rows on tile boundaries), or staged into the landing
+    # buffer when a source is not 16-byte aligned or lies in pinned host
+    # memory; the landing buffer starts as NaN, so a partial read from the
+    # wrong place shows
+    n = 4
+    M, N, K = 1024, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=98)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    rows = M // n
+    r = 2
+    _say("rs first-step partials", ring, source)
+    case = RSCase(inp, r, ring, pinned_remote=source == "pinned")
+    keep = None
+    if source == "misaligned":
+        # every partial one float into a larger buffer: 4-byte but not 16-byte aligned
+        keep = [torch.empty(rows * N + 4, dtype=torch.float32, device="cuda") for _ in range(n)]
+        for c in range(n):
+            keep[c][1:1 + rows * N].copy_(case.partials[c].reshape(-1))
+        case.partials = [keep[c][1:1 + rows * N].view(rows, N) for c in range(n)]
+        case.problem = C.rs_problem(case.A, case.W, case.partials, case.stage, case.C, case.send, r, ring)
+    case.stage.fill_(float("nan"))
+    torch.cuda.synchronize()
+    C.compass_gemm_rs(case.problem, C.links(40e9, 10e9, slice_bytes=1 << 18))
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), ref)
+    for q in range(n):
+        if q != r:
+            assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
+
+
 def test_gemm_rs_random_ragged_no_sends():
     n = 4
     M, N, K = 1024, 776, 1032
