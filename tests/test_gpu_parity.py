@@ -110,6 +110,36 @@ def test_split_k_random_close_to_unsplit():
     assert rel_err(out[7], out[3]) < 2.0 ** -7
 
 
+@pytest.mark.parametrize("K,slices", [(2560, 5), (3072, 6), (3584, 7), (4096, 8)])
+@pytest.mark.parametrize("partial", [False, True])
+def test_split_k_five_to_eight_slices_integer_exact(K, slices, partial):
+    # a 256 x 256 plain GEMM is four 128 x 128 tiles on 512 workgroup slots:
+    # K splits into as many 512-deep slices as it holds, up to 8, so these
+    # depths reach the completing slice's instances for 5 to 8 slices (with
+    # the fp32 partial: the ReduceScatter variant's); the tile trace counts
+    # the slices
+    M, N = 256, 256
+    inp = make_int_rs_inputs(M, N, K, 1, seed=70 + slices)
+    A, W = dev_bits(inp["A"]), dev_bits(inp["W"])
+    prod = O.ag_gemm([O.bf16_to_f64(inp["A"])], O.bf16_to_f64(inp["W"]))
+    P = None
+    if partial:
+        P = torch.from_numpy(np.ascontiguousarray(inp["P_in"][0], dtype=np.float32)).cuda()
+        prod = prod + inp["P_in"][0].astype(np.float64)
+    ref = O.f64_to_bf16_rne(prod)
+    Cm = torch.full((M, N), 0x7FC0, dtype=torch.int16, device="cuda")
+    _say("split k slices", slices, partial)
+    C.compass_set_option(C.OPT_TILE_TRACE, 1024)
+    try:
+        C.compass_gemm(A, W, Cm, P)
+        torch.cuda.synchronize()
+        rec = C.compass_tile_trace(1024)
+    finally:
+        C.compass_set_option(C.OPT_TILE_TRACE, 0)
+    assert len(rec) == 4 * slices
+    assert np.array_equal(host_bits(Cm), ref)
+
+
 def test_decomp_d16_split_integer_exact():
     # sub-GEMMs of 64 rows: one row tile each, K split
     n, d = 8, 16
