@@ -138,4 +138,65 @@ __host__ __device__ inline int work_items(const GemmParams &p) {
     return p.head_tiles * p.head_split + (p.split_from - p.head_tiles) + (tiles - p.split_from) * p.ksplit;
 }
 
+// One work item: the tile at position `tpos` of the ready order and, when
+// its K is split (`split`), slice `slice` of `ns`, covering K from
+// slice * ksl (at most ksl deep), counted by split counter `uc`, its
+// partial at workspace tile wsf + slice (the tile's slices at [wsf,
+// wsf + ns)). An unsplit tile runs its whole K (slice 0 of 1).
+struct WorkItem {
+    int tpos, slice, ns, uc, wsf, ksl;
+    bool split;
+};
+
+// Work position -> work item: positions [0, head_tiles * head_split) are
+// the head's slices (tile u = pos / head_split), then the whole tiles up to
+// tile position split_from, then the tail's slices (ksplit per tile).
+__host__ __device__ inline WorkItem decode_item(const GemmParams &p, int pos) {
+    const int head_items = p.head_tiles * p.head_split;
+    WorkItem w;
+    w.slice = 0;
+    w.ns = 1;
+    w.uc = 0;
+    w.wsf = 0;
+    w.ksl = p.K;
+    w.split = false;
+    if (pos < head_items) {
+        w.uc = pos / p.head_split;
+        w.slice = pos - w.uc * p.head_split;
+        w.tpos = w.uc;
+        w.split = true;
+        w.ns = p.head_split;
+        w.wsf = w.uc * p.head_split;
+        w.ksl = p.head_kslice;
+    } else {
+        const int q = pos - head_items + p.head_tiles;   // position in the unsplit-head order
+        if (p.ksplit > 1 && q >= p.split_from) {
+            const int u = (q - p.split_from) / p.ksplit;
+            w.slice = q - p.split_from - u * p.ksplit;
+            w.tpos = p.split_from + u;
+            w.split = true;
+            w.ns = p.ksplit;
+            w.uc = p.head_tiles + u;
+            w.wsf = head_items + u * p.ksplit;
+            w.ksl = p.kslice;
+        } else {
+            w.tpos = q;
+        }
+    }
+    return w;
+}
+
+// Tile position -> (row-tile ordinal in rt_order, column tile): positions
+// walk group_m row tiles (fewer in a last, partial group) before the next
+// column tile.
+__host__ __device__ inline void tile_of(const GemmParams &p, int tpos, int *ti, int *tn) {
+    const int gsz = p.group_m * p.tiles_n;
+    const int grp = tpos / gsz;
+    const int rin = tpos - grp * gsz;
+    const int left = p.tiles_m - grp * p.group_m;
+    const int rows_here = p.group_m < left ? p.group_m : left;
+    *ti = grp * p.group_m + rin % rows_here;
+    *tn = rin / rows_here;
+}
+
 }  // namespace compass

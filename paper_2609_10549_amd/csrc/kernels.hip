@@ -317,7 +317,6 @@ void gemm_kernel(const GemmParams p) {
     const int wm0 = (wave >> 1) * WM;
     const int wn0 = (wave & 1) * WN;
     const int total = work_items(p);
-    const int head_items = p.head_tiles * p.head_split;
     const int v = p.nq > 1 ? (int)(blockIdx.x % (uint32_t)p.nq) : 0;
 
 
@@ -353,40 +352,14 @@ void gemm_kernel(const GemmParams p) {
         // work position -> (tile position, K slice); `split`: this tile's K
         // is split into `ns` slices, counted by split_cnt[uc], its partials
         // at workspace tiles [wsf, wsf + ns)
-        bool split = false;
-        int tpos, slice = 0, ns = 1, uc = 0, wsf = 0, ksl = p.K;
-        if (pos < head_items) {
-            uc = pos / p.head_split;
-            slice = pos - uc * p.head_split;
-            tpos = uc;
-            split = true;
-            ns = p.head_split;
-            wsf = uc * p.head_split;
-            ksl = p.head_kslice;
-        } else {
-            const int q = pos - head_items + p.head_tiles;   // position in the unsplit-head order
-            if (p.ksplit > 1 && q >= p.split_from) {
-                const int u = (q - p.split_from) / p.ksplit;
-                slice = q - p.split_from - u * p.ksplit;
-                tpos = p.split_from + u;
-                split = true;
-                ns = p.ksplit;
-                uc = p.head_tiles + u;
-                wsf = head_items + u * p.ksplit;
-                ksl = p.kslice;
-            } else {
-                tpos = q;
-            }
-        }
+        const WorkItem wi = decode_item(p, pos);
+        const bool split = wi.split;
+        const int tpos = wi.tpos, slice = wi.slice, ns = wi.ns, uc = wi.uc, wsf = wi.wsf, ksl = wi.ksl;
         const int kb = split ? slice * ksl : 0;
         const int ke = split ? min(p.K, kb + ksl) : p.K;
         // tile position -> (row-tile ordinal, column tile): group_m rows at a time
-        const int gsz = p.group_m * p.tiles_n;
-        const int grp = tpos / gsz;
-        const int rin = tpos - grp * gsz;
-        const int rows_here = min(p.group_m, p.tiles_m - grp * p.group_m);
-        const int ti = grp * p.group_m + rin % rows_here;
-        const int tn = rin / rows_here;
+        int ti, tn;
+        tile_of(p, tpos, &ti, &tn);
         const int rt = p.rt_order[ti];
         const int m0 = rt * BM;
         const int n0 = tn * BN;
