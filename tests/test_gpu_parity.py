@@ -343,6 +343,30 @@ def test_gemm_rs_first_step_partial_sources_integer_exact(ring, source):
             assert np.array_equal(host_bits(case.send[q]), ref[q * rows:(q + 1) * rows]), f"send {q}"
 
 
+@pytest.mark.parametrize("ring", ["single", "double"])
+def test_gemm_rs_pinned_host_partials_and_sends_integer_exact(ring):
+    # every remote buffer of the ReduceScatter in pinned host memory: the
+    # incoming partials (the first step's staged, the others copied by the
+    # engines across PCIe) and every chunk sent on
+    n = 4
+    M, N, K = 1024, 264, 136
+    inp = make_int_rs_inputs(M, N, K, n, seed=99)
+    ref = O.f64_to_bf16_rne(O.gemm_rs(O.bf16_to_f64(inp["A"]), O.bf16_to_f64(inp["W"]),
+                                      [p.astype(np.float64) for p in inp["P_in"]], n))
+    rows = M // n
+    r = 1
+    _say("rs pinned partials and sends", ring)
+    case = RSCase(inp, r, ring, pinned_remote=True)
+    case.send = [None if q == r else torch.zeros((rows, N), dtype=torch.int16, pin_memory=True) for q in range(n)]
+    case.problem = C.rs_problem(case.A, case.W, case.partials, case.stage, case.C, case.send, r, ring)
+    C.compass_gemm_rs(case.problem, C.links(40e9, 10e9, slice_bytes=1 << 18))
+    C.compass_sync()
+    assert np.array_equal(host_bits(case.C), ref)
+    for q in range(n):
+        if q != r:
+            assert np.array_equal(case.send[q].numpy().view(np.uint16), ref[q * rows:(q + 1) * rows]), f"send {q}"
+
+
 def test_gemm_rs_random_ragged_no_sends():
     n = 4
     M, N, K = 1024, 776, 1032
